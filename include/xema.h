@@ -1,0 +1,192 @@
+/*
+ * xema.h -- C ABI of the DiT block forward for AMD Instinct MI355X (gfx950).
+ *
+ * One call runs one Diffusion-Transformer denoising-step block: the stage the
+ * paper identifies as dominating diffusion inference (Sec. 2.1: the denoiser
+ * is a stack of repeated transformer blocks), whose activations grow with the
+ * latent sequence length H x W x T (Sec. 2.2), token-chunked under a per-call
+ * activation budget.  Chunking is the paper's "only as much mitigation as
+ * needed" (Sec. 5.1, objective pi*) applied to the operators it names for
+ * chunking, DiT attention and its neighbours (Sec. 5.2, "Localized chunking
+ * and fusion"; Sec. 8, memory mitigation primitives).  All intermediates live
+ * in one caller-owned arena at offsets fixed offline by the paper's static
+ * layout, Algorithm 1 (Sec. 6.1), so runtime allocation is a table lookup
+ * (Sec. 8, "Static memory runtime").
+ *
+ * Conventions for every function here:
+ *   - Return value: XEMA_OK (0) or a negative xema_status.  Nothing throws.
+ *   - Every argument is validated on the host before any device work; on an
+ *     error no kernel has been launched and no output byte was written.
+ *   - The library never allocates or frees device memory and keeps no global
+ *     device state.  All functions are thread-safe.
+ *   - Device pointers must be 16-byte aligned; the workspace 256-byte aligned.
+ *   - Token/weight/conditioning inputs are bfloat16 (bit patterns, uint16).
+ */
+#ifndef XEMA_H_
+#define XEMA_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  XEMA_OK = 0,
+  XEMA_ERR_INVALID_ARG = -1,          /* NULL pointer, non-positive size, aliasing */
+  XEMA_ERR_UNSUPPORTED = -2,          /* shape outside what the kernels handle */
+  XEMA_ERR_BUDGET_TOO_SMALL = -3,     /* even the smallest chunk exceeds the budget */
+  XEMA_ERR_WORKSPACE_TOO_SMALL = -4,  /* workspace_bytes below the plan's arena size */
+  XEMA_ERR_MISALIGNED = -5,           /* pointer alignment violated */
+  XEMA_ERR_HIP = -6                   /* a HIP launch or runtime call failed */
+} xema_status;
+
+#define XEMA_MAX_SLOTS 16
+#define XEMA_CHUNK_GRANULE 256        /* planned chunks are multiples of this, or all */
+#define XEMA_SEQ_PAD 128              /* per-head Q/K/V storage pads L to this */
+
+/* Block hyper-parameters: the "model" part of a request template
+ * r = (model, H, W, T) (Sec. 2.1).
+ *   hidden      D = heads * head_dim, a multiple of 256, at most 8192
+ *   heads       H
+ *   head_dim    d, 64 or 128
+ *   mlp_hidden  F, a multiple of 256
+ *   cond_dim    D_c, width of the conditioning vector, a multiple of 8
+ *   rope_dims   (d_t, d_h, d_w): even widths of the contiguous [t | y | w]
+ *               RoPE segments of each head vector, sum <= head_dim
+ *   rope_theta  RoPE base (10000 in every shipped config)
+ *   ln_eps      LayerNorm epsilon; qk_eps  QK-RMSNorm epsilon            */
+typedef struct {
+  int32_t hidden, heads, head_dim, mlp_hidden, cond_dim;
+  int32_t rope_dims[3];
+  float rope_theta, ln_eps, qk_eps;
+} xema_block_cfg;
+
+/* One batched call: `batch` requests of one template (the paper batches only
+ * within a template, Sec. 2.3 "Concurrency"), each a sequence of text_len text
+ * tokens followed by grid_t * grid_h * grid_w visual tokens in t-major, then
+ * row, then column order.  L = text_len + grid_t * grid_h * grid_w.        */
+typedef struct {
+  int32_t batch, text_len, grid_t, grid_h, grid_w;
+} xema_request;
+
+/* Device pointers to the block weights, bfloat16, nn.Linear layout [out, in]:
+ *   ada_w [6D, D_c]  ada_b [6D]     AdaLN map, rows ordered (shift1, scale1,
+ *                                   gate1, shift2, scale2, gate2)
+ *   qkv_w [3D, D]    qkv_b [3D]     rows ordered (q | k | v), head j owns rows
+ *                                   [j d, (j+1) d) of each part
+ *   q_gamma [d]      k_gamma [d]    QK-RMSNorm gains shared by all heads
+ *   o_w [D, D]       o_b [D]        attention output projection
+ *   up_w [F, D]      up_b [F]       MLP up projection (GELU-tanh follows)
+ *   down_w [D, F]    down_b [D]     MLP down projection                    */
+typedef struct {
+  const void *ada_w, *ada_b, *qkv_w, *qkv_b, *q_gamma, *k_gamma;
+  const void *o_w, *o_b, *up_w, *up_b, *down_w, *down_b;
+} xema_block_weights;
+
+/* A static arena layout: the tensor-id -> offset table of Sec. 8 ("Static
+ * memory runtime") produced by Algorithm 1 (Sec. 6.1) over the block's slot
+ * lifetimes.  slot_begin/slot_end are half-open step lifetimes.           */
+typedef struct {
+  int32_t chunk_tokens;               /* tokens per sequence per chunk; == L means unchunked */
+  int32_t n_slots;
+  int64_t workspace_bytes;            /* arena size at chunk_tokens (Algorithm 1 peak) */
+  int64_t min_workspace_bytes;        /* arena size at the smallest candidate chunk */
+  int64_t slot_offset[XEMA_MAX_SLOTS];
+  int64_t slot_bytes[XEMA_MAX_SLOTS];
+  int32_t slot_begin[XEMA_MAX_SLOTS];
+  int32_t slot_end[XEMA_MAX_SLOTS];
+} xema_plan;
+
+/* Slot ids of xema_plan.  Steps: 0 AdaLN map + RoPE table; phase A (per token
+ * chunk) 1 LN1, 2 QKV projection, 3 QK-norm/RoPE scatter; 4 fp16 copies of the
+ * phase-B weights; phase B (per query chunk) 5 attention, 6 out-projection +
+ * gated residual, 7 LN2, 8 MLP up + GELU, 9 MLP down + gated residual.     */
+enum {
+  XEMA_SLOT_MOD = 0,   /* fp32 [B, 6D]                      life [0, 10) */
+  XEMA_SLOT_ROPE,      /* fp32 cos/sin per axis position     life [0, 4)  */
+  XEMA_SLOT_Q,         /* fp16 [B, H, Lp, d]                 life [1, 10) */
+  XEMA_SLOT_K,         /* fp16 [B, H, Lp, d]                 life [1, 10) */
+  XEMA_SLOT_VT,        /* fp16 [B, H, d, Lp] (transposed)    life [1, 10) */
+  XEMA_SLOT_LN1,       /* bf16 [B*c, D]                      life [1, 3)  */
+  XEMA_SLOT_QKV,       /* fp16 [B*c, 3D]                     life [2, 4)  */
+  XEMA_SLOT_WO16,      /* fp16 [D, D]                        life [4, 10) */
+  XEMA_SLOT_WUP16,     /* fp16 [F, D]                        life [4, 10) */
+  XEMA_SLOT_WDOWN16,   /* fp16 [D, F]                        life [4, 10) */
+  XEMA_SLOT_ATTN,      /* fp16 [B*c, D]                      life [5, 7)  */
+  XEMA_SLOT_X1,        /* fp32 [B*c, D]                      life [6, 10) */
+  XEMA_SLOT_LN2,       /* fp16 [B*c, D]                      life [7, 9)  */
+  XEMA_SLOT_HID,       /* fp16 [B*c, F]                      life [8, 10) */
+  XEMA_NUM_SLOTS
+};
+
+/* Fill `out` from a request template r = (model, H, W, T) (Sec. 2.1): the
+ * latent grid is grid_h = ceil(H / 16), grid_w = ceil(W / 16) (8x spatial VAE
+ * downsampling and 2x2 patches) and grid_t = (T - 1) / 4 + 1 (4x temporal VAE
+ * downsampling; T = 1 is an image).  Host only.
+ * Errors: XEMA_ERR_INVALID_ARG for NULL pointers or non-positive sizes.     */
+int xema_request_from_template(const xema_block_cfg* cfg, int32_t height, int32_t width,
+                               int32_t frames, int32_t batch, int32_t text_len,
+                               xema_request* out);
+
+/* Arena layout for a given chunk size (chunk_tokens <= 0 or >= L means
+ * unchunked): slot sizes and lifetimes of the block, packed by Algorithm 1
+ * (Sec. 6.1).  Host only.
+ * Errors: XEMA_ERR_INVALID_ARG, XEMA_ERR_UNSUPPORTED (shape checks).       */
+int xema_workspace_layout(const xema_block_cfg* cfg, const xema_request* req,
+                          int32_t chunk_tokens, xema_plan* out);
+
+/* Arena bytes needed at chunk_tokens (the layout's workspace_bytes).  Host only. */
+int xema_workspace_bytes(const xema_block_cfg* cfg, const xema_request* req,
+                         int32_t chunk_tokens, int64_t* bytes);
+
+/* "Only as much mitigation as needed" (Sec. 5.1, pi*): the largest candidate
+ * chunk (L itself, or a multiple of XEMA_CHUNK_GRANULE below L) whose arena
+ * fits budget_bytes, with its layout.  The budget counts arena bytes only;
+ * caller-owned tokens, weights, conditioning and output are not in it.
+ * Host only.
+ * Errors: XEMA_ERR_BUDGET_TOO_SMALL when no candidate fits (out->chunk_tokens
+ * is then 0 and out->min_workspace_bytes holds the smallest arena);
+ * XEMA_ERR_INVALID_ARG, XEMA_ERR_UNSUPPORTED.                              */
+int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* req,
+                        int64_t budget_bytes, xema_plan* out);
+
+/* One DiT block forward, asynchronous on `stream` (a hipStream_t; NULL means
+ * the default stream).
+ *   tokens   device, bf16 [B, L, D] row-major, read only
+ *   weights  device pointers, see xema_block_weights
+ *   cond     device, bf16 [B, D_c], the conditioning vector of each request
+ *   chunk_tokens  tokens per sequence per chunk for both phases; <= 0 or >= L
+ *            means unchunked; any positive value is accepted (the last chunk
+ *            may be shorter).  The result is bit-identical for every value.
+ *   workspace, workspace_bytes  device arena of at least
+ *            xema_workspace_bytes(cfg, req, chunk_tokens) bytes, 256-byte
+ *            aligned, owned by the caller.  Its contents on entry are ignored;
+ *            on return it holds the intermediates at the layout's offsets.
+ *   out      device, fp32 [B, L, D], written once per element; must not
+ *            overlap tokens, weights, cond or the workspace.
+ * Computes, per batch element (the block definition: AdaLN-modulated
+ * LayerNorm, QKV projection, QK-RMSNorm, 3D RoPE, joint full self-attention,
+ * gated output projection, LayerNorm, GELU-tanh MLP, gated residual):
+ *   m = W_ada c + b_ada = (shift1, scale1, gate1, shift2, scale2, gate2)
+ *   h = LN(x)(1 + scale1) + shift1;  [q|k|v] = h W_qkv^T + b_qkv
+ *   q, k <- RoPE(RMSNorm(.) * gamma) per head;  o = softmax(q k^T / sqrt(d)) v
+ *   x1 = x + gate1 (o W_o^T + b_o);  h2 = LN(x1)(1 + scale2) + shift2
+ *   out = x1 + gate2 (GELU_tanh(h2 W_up^T + b_up) W_down^T + b_down)
+ * Errors (all raised before any launch): XEMA_ERR_INVALID_ARG,
+ * XEMA_ERR_UNSUPPORTED, XEMA_ERR_MISALIGNED, XEMA_ERR_WORKSPACE_TOO_SMALL;
+ * XEMA_ERR_HIP if a launch fails.                                          */
+int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
+                       const void* tokens, const xema_block_weights* weights,
+                       const void* cond, int32_t chunk_tokens,
+                       void* workspace, int64_t workspace_bytes,
+                       void* out, void* stream);
+
+/* Static string naming a status code. */
+const char* xema_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XEMA_H_ */
