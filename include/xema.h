@@ -31,6 +31,8 @@
 extern "C" {
 #endif
 
+#define XEMA_API __attribute__((visibility("default")))
+
 typedef enum {
   XEMA_OK = 0,
   XEMA_ERR_INVALID_ARG = -1,          /* NULL pointer, non-positive size, aliasing */
@@ -125,7 +127,7 @@ enum {
  * downsampling and 2x2 patches) and grid_t = (T - 1) / 4 + 1 (4x temporal VAE
  * downsampling; T = 1 is an image).  Host only.
  * Errors: XEMA_ERR_INVALID_ARG for NULL pointers or non-positive sizes.     */
-int xema_request_from_template(const xema_block_cfg* cfg, int32_t height, int32_t width,
+XEMA_API int xema_request_from_template(const xema_block_cfg* cfg, int32_t height, int32_t width,
                                int32_t frames, int32_t batch, int32_t text_len,
                                xema_request* out);
 
@@ -133,11 +135,11 @@ int xema_request_from_template(const xema_block_cfg* cfg, int32_t height, int32_
  * unchunked): slot sizes and lifetimes of the block, packed by Algorithm 1
  * (Sec. 6.1).  Host only.
  * Errors: XEMA_ERR_INVALID_ARG, XEMA_ERR_UNSUPPORTED (shape checks).       */
-int xema_workspace_layout(const xema_block_cfg* cfg, const xema_request* req,
+XEMA_API int xema_workspace_layout(const xema_block_cfg* cfg, const xema_request* req,
                           int32_t chunk_tokens, xema_plan* out);
 
 /* Arena bytes needed at chunk_tokens (the layout's workspace_bytes).  Host only. */
-int xema_workspace_bytes(const xema_block_cfg* cfg, const xema_request* req,
+XEMA_API int xema_workspace_bytes(const xema_block_cfg* cfg, const xema_request* req,
                          int32_t chunk_tokens, int64_t* bytes);
 
 /* "Only as much mitigation as needed" (Sec. 5.1, pi*): the largest candidate
@@ -148,7 +150,7 @@ int xema_workspace_bytes(const xema_block_cfg* cfg, const xema_request* req,
  * Errors: XEMA_ERR_BUDGET_TOO_SMALL when no candidate fits (out->chunk_tokens
  * is then 0 and out->min_workspace_bytes holds the smallest arena);
  * XEMA_ERR_INVALID_ARG, XEMA_ERR_UNSUPPORTED.                              */
-int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* req,
+XEMA_API int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* req,
                         int64_t budget_bytes, xema_plan* out);
 
 /* One DiT block forward, asynchronous on `stream` (a hipStream_t; NULL means
@@ -176,14 +178,14 @@ int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* req,
  * Errors (all raised before any launch): XEMA_ERR_INVALID_ARG,
  * XEMA_ERR_UNSUPPORTED, XEMA_ERR_MISALIGNED, XEMA_ERR_WORKSPACE_TOO_SMALL;
  * XEMA_ERR_HIP if a launch fails.                                          */
-int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
+XEMA_API int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
                        const void* tokens, const xema_block_weights* weights,
                        const void* cond, int32_t chunk_tokens,
                        void* workspace, int64_t workspace_bytes,
                        void* out, void* stream);
 
 /* Static string naming a status code. */
-const char* xema_status_str(int status);
+XEMA_API const char* xema_status_str(int status);
 
 #ifdef __cplusplus
 }

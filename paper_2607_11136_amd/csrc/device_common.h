@@ -1,0 +1,58 @@
+// Device-side helpers for the gfx950 kernels of libxema.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace xema {
+
+typedef _Float16 f16;
+typedef __bf16 bf16;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// LDS address-space pointer, as taken by the direct global->LDS load builtin.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
+
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+__device__ __forceinline__ float to_f32(f16 x) { return (float)x; }
+__device__ __forceinline__ float to_f32(float x) { return x; }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+template <>
+__device__ __forceinline__ f16 from_f32<f16>(float x) { return (f16)x; }
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+
+// Butterfly sum over the 64 lanes of a wave (fixed pairing order, so every
+// lane ends with the same, run-to-run reproducible value).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// GELU, tanh form: 0.5 u (1 + tanh(a (u + 0.044715 u^3))), a = sqrt(2/pi),
+// written with tanh(z) = 1 - 2 / (exp(2z) + 1).
+__device__ __forceinline__ float gelu_tanh(float u) {
+  const float a = 0.7978845608028654f;
+  const float z = a * fmaf(0.044715f * u, u * u, u);
+  const float e = __expf(2.0f * z);
+  const float t = 1.0f - 2.0f / (e + 1.0f);
+  return 0.5f * u * (1.0f + t);
+}
+
+}  // namespace xema

@@ -1,0 +1,73 @@
+// Launch functions of the gfx950 kernels (host-callable, asynchronous).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "xema_ops.h"
+
+namespace xema {
+
+struct RowMap {
+  int64_t rows_per_batch, batch_stride, row_offset;
+};
+
+struct RopeGeom {
+  int grid[3];  // (G_t, G_h, G_w)
+  int dims[3];  // (d_t, d_h, d_w)
+};
+
+struct QkRopeArgs {
+  const _Float16* qkv;
+  const uint16_t* q_gamma;
+  const uint16_t* k_gamma;
+  const float2* table;
+  _Float16* q;
+  _Float16* k;
+  _Float16* vt;
+  int batch, heads, text_len, padded_len;
+  int tok_begin, tok_count, count_ext;  // count_ext adds the zeroed padding tokens
+  float qk_eps;
+  RopeGeom geom;
+};
+
+struct GemmParams {
+  int dtype;  // XEMA_BF16 / XEMA_F16 operands
+  const void* a;
+  const void* b;
+  int64_t M;
+  int N, K;
+  const uint16_t* bias;
+  int epilogue;
+  void* c;
+  int c_dtype;
+  RowMap c_map;
+  int64_t ldc;
+  const void* resid;
+  int resid_dtype;
+  RowMap resid_map;
+  int64_t ld_resid;
+  const float* gate;
+  int64_t gate_stride;
+};
+
+struct AttnParams {
+  const _Float16* q;
+  const _Float16* k;
+  const _Float16* vt;
+  _Float16* o;
+  int batch, heads, seq_len, padded_len, q_begin, q_count;
+};
+
+hipError_t launch_adaln(const uint16_t* cond, const uint16_t* w, const uint16_t* bias, int batch,
+                        int cond_dim, int out_dim, float* mod, hipStream_t s);
+hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows, int dim,
+                              const float* shift, const float* scale, int64_t mod_stride,
+                              float eps, void* y, int y_dtype, hipStream_t s);
+hipError_t launch_rope_table(RopeGeom g, float theta, float* table, hipStream_t s);
+hipError_t launch_qk_norm_rope(const QkRopeArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_convert_f16(const uint16_t* src, _Float16* dst, int64_t n, hipStream_t s);
+hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
+hipError_t launch_attention(const AttnParams& p, int head_dim, hipStream_t s);
+
+}  // namespace xema

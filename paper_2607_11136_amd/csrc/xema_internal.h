@@ -1,0 +1,33 @@
+// Internal declarations shared by the host-side sources of libxema.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include "xema.h"
+#include "xema_ops.h"
+
+namespace xema {
+
+constexpr int64_t kAlign = 256;
+
+inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+inline int64_t seq_len(const xema_request& r) {
+  return (int64_t)r.text_len + (int64_t)r.grid_t * r.grid_h * r.grid_w;
+}
+inline int64_t padded_len(int64_t L) { return round_up(L, XEMA_SEQ_PAD); }
+
+// Shape checks shared by planning and the forward call.
+int validate_shapes(const xema_block_cfg* cfg, const xema_request* req);
+
+// Chunk size actually used for a requested chunk_tokens.
+inline int64_t effective_chunk(int64_t L, int64_t chunk) {
+  return (chunk <= 0 || chunk >= L) ? L : chunk;
+}
+
+// Fill `out` with the slot table at chunk `c` and its Algorithm 1 offsets.
+int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
+                     xema_plan* out);
+
+}  // namespace xema

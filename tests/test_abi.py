@@ -1,0 +1,201 @@
+"""C ABI checks that need no GPU: the library loads and exports every symbol
+the headers declare; the C++ planner (Algorithm 1 + chunk plan) matches the
+Python oracle byte for byte; host-side validation returns the documented
+status codes before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_11136_amd as X
+import workloads as W
+from oracle import layout as OL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _cfg(s: W.BlockShape):
+    return X.block_cfg(s.hidden, s.heads, s.head_dim, s.mlp_hidden, s.cond_dim, s.rope_dims,
+                       s.rope_theta, s.ln_eps, s.qk_eps)
+
+
+def _req(s: W.BlockShape):
+    return X.request(s.batch, s.text_len, *s.grid)
+
+
+def _declared_symbols():
+    names = set()
+    for h in ("xema.h", "xema_ops.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        names.update(re.findall(r"XEMA_API\s+[\w\s\*]+?\b(xema_\w+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = X.lib()
+    declared = _declared_symbols()
+    assert len(declared) == 13, declared
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert declared == set(X.EXPORTED)
+
+
+def test_status_strings():
+    assert X.xema_status_str(0) == "ok"
+    assert "budget" in X.xema_status_str(X.XEMA_ERR_BUDGET_TOO_SMALL)
+
+
+@pytest.mark.parametrize("name", sorted(W.CONFIGS))
+def test_layout_matches_oracle(name):
+    s = W.CONFIGS[name]
+    for chunk in sorted({0, 1, 64, 100, 256, 2048, 8192} | set(s.chunks)):
+        p = X.xema_workspace_layout(_cfg(s), _req(s), chunk)
+        ts = OL.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, chunk)
+        offs, peak = OL.static_layout(ts)
+        assert p.n_slots == len(ts) == len(X.SLOT_NAMES)
+        assert p.workspace_bytes == peak
+        assert list(p.slot_offset[:p.n_slots]) == offs
+        assert list(p.slot_bytes[:p.n_slots]) == [OL.round_up(t.size, OL.ALIGN) for t in ts]
+        assert list(p.slot_begin[:p.n_slots]) == [t.begin for t in ts]
+        assert list(p.slot_end[:p.n_slots]) == [t.end for t in ts]
+        c = s.seq_len if chunk <= 0 or chunk >= s.seq_len else chunk
+        assert p.chunk_tokens == c
+        assert X.xema_workspace_bytes(_cfg(s), _req(s), chunk) == peak
+
+
+@pytest.mark.parametrize("name", ["tiny", "video", "highres", "long"])
+def test_plan_matches_oracle(name):
+    s = W.CONFIGS[name]
+    smallest = OL.workspace_bytes(s, OL.chunk_candidates(s.seq_len)[-1])
+    full = OL.workspace_bytes(s, 0)
+    for budget in sorted({smallest, smallest + 12345, (smallest + full) // 2, full - 1, full,
+                          32 * 10**9}):
+        c, ws, small = OL.plan(s, budget)
+        p = X.xema_workspace_plan(_cfg(s), _req(s), budget)
+        assert (p.chunk_tokens, p.workspace_bytes, p.min_workspace_bytes) == (c, ws, small)
+
+
+def test_plan_budget_too_small_reports_minimum():
+    s = W.HIGHRES
+    smallest = OL.workspace_bytes(s, 256)
+    with pytest.raises(X.XemaError) as e:
+        X.xema_workspace_plan(_cfg(s), _req(s), smallest - 1)
+    assert e.value.status == X.XEMA_ERR_BUDGET_TOO_SMALL
+    assert e.value.plan.min_workspace_bytes == smallest
+    assert e.value.plan.chunk_tokens == 0
+
+
+def test_highres_32gb_budget_runs_unchunked():
+    s = W.HIGHRES
+    p = X.xema_workspace_plan(_cfg(s), _req(s), 32 * 2**30)
+    assert p.chunk_tokens == s.seq_len
+    assert p.workspace_bytes <= 32 * 2**30
+
+
+@pytest.mark.parametrize("hwt,grid", [((1024, 1024, 1), (1, 64, 64)), ((480, 720, 49), (13, 30, 45)),
+                                      ((1080, 1920, 49), (13, 68, 120)), ((352, 608, 129), (33, 22, 38))])
+def test_request_from_template(hwt, grid):
+    r = X.xema_request_from_template(_cfg(W.VIDEO), *hwt, 1, 226)
+    assert (r.grid_t, r.grid_h, r.grid_w) == grid
+    assert (r.batch, r.text_len) == (1, 226)
+
+
+def _bad_cfg(**kw):
+    s = W.TINY
+    c = _cfg(s)
+    for k, v in kw.items():
+        if k == "rope_dims":
+            for i in range(3):
+                c.rope_dims[i] = v[i]
+        else:
+            setattr(c, k, v)
+    return c
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"head_dim": 32, "heads": 8, "rope_dims": (8, 12, 12)}, X.XEMA_ERR_UNSUPPORTED),
+    ({"heads": 3}, X.XEMA_ERR_INVALID_ARG),
+    ({"hidden": 320, "heads": 5}, X.XEMA_ERR_UNSUPPORTED),
+    ({"mlp_hidden": 1000}, X.XEMA_ERR_UNSUPPORTED),
+    ({"rope_dims": (16, 24, 25)}, X.XEMA_ERR_INVALID_ARG),
+    ({"rope_dims": (32, 24, 24)}, X.XEMA_ERR_INVALID_ARG),
+    ({"ln_eps": 0.0}, X.XEMA_ERR_INVALID_ARG),
+    ({"cond_dim": 12}, X.XEMA_ERR_UNSUPPORTED),
+])
+def test_bad_shapes_rejected(kw, status):
+    with pytest.raises(X.XemaError) as e:
+        X.xema_workspace_layout(_bad_cfg(**kw), _req(W.TINY), 0)
+    assert e.value.status == status
+
+
+def test_bad_request_rejected():
+    for r in (X.request(0, 32, 1, 16, 16), X.request(1, -1, 1, 16, 16), X.request(1, 0, 0, 0, 0)):
+        with pytest.raises(X.XemaError) as e:
+            X.xema_workspace_layout(_cfg(W.TINY), r, 0)
+        assert e.value.status == X.XEMA_ERR_INVALID_ARG
+
+
+# Host-side validation of the forward call.  The addresses below are never
+# dereferenced: every case fails validation before any HIP call.
+BASE = 1 << 40
+
+
+def _fake_call(s, chunk=0, ws_bytes=None, ws_addr=None, out_addr=None, tok_addr=None, w_over=None):
+    cfg, req = _cfg(s), _req(s)
+    need = X.xema_workspace_bytes(cfg, req, chunk)
+    ws_bytes = need if ws_bytes is None else ws_bytes
+    addr = BASE
+    tok = BASE + (1 << 34) if tok_addr is None else tok_addr
+    out = BASE + (2 << 34) if out_addr is None else out_addr
+    ws = BASE + (3 << 34) if ws_addr is None else ws_addr
+    cond = BASE + (4 << 34)
+    w = X.BlockWeights()
+    for i, n in enumerate(X.WEIGHT_FIELDS):
+        setattr(w, n, BASE + (5 << 34) + i * (1 << 30))
+    for k, v in (w_over or {}).items():
+        setattr(w, k, v)
+    return X.lib().xema_dit_block_fwd(ctypes.byref(cfg), ctypes.byref(req), tok, ctypes.byref(w),
+                                      cond, chunk, ws, ws_bytes, out, None)
+
+
+def test_fwd_workspace_too_small():
+    assert _fake_call(W.TINY, ws_bytes=1000) == X.XEMA_ERR_WORKSPACE_TOO_SMALL
+    need64 = X.xema_workspace_bytes(_cfg(W.TINY), _req(W.TINY), 64)
+    assert _fake_call(W.TINY, chunk=0, ws_bytes=need64) == X.XEMA_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_fwd_misaligned():
+    assert _fake_call(W.TINY, ws_addr=BASE + (3 << 34) + 128) == X.XEMA_ERR_MISALIGNED
+    assert _fake_call(W.TINY, out_addr=BASE + (2 << 34) + 8) == X.XEMA_ERR_MISALIGNED
+    assert _fake_call(W.TINY, w_over={"qkv_w": BASE + (9 << 34) + 4}) == X.XEMA_ERR_MISALIGNED
+
+
+def test_fwd_aliasing_rejected():
+    # out overlapping tokens, or the workspace overlapping a weight
+    assert _fake_call(W.TINY, out_addr=BASE + (1 << 34) + 4096) == X.XEMA_ERR_INVALID_ARG
+    assert _fake_call(W.TINY, w_over={"o_w": BASE + (3 << 34) + 1024}) == X.XEMA_ERR_INVALID_ARG
+    assert _fake_call(W.TINY, w_over={"down_b": None}) == X.XEMA_ERR_INVALID_ARG
+
+
+def test_op_validation():
+    L = X.lib()
+    f = BASE
+    # attention: head_dim 96 unsupported; padded_len not a multiple of 128
+    assert L.xema_op_attention(f, f, f, 1, 4, 96, 300, 384, 0, 300, f + (1 << 30), None) == X.XEMA_ERR_UNSUPPORTED
+    assert L.xema_op_attention(f, f, f, 1, 4, 64, 300, 320, 0, 300, f + (1 << 30), None) == X.XEMA_ERR_UNSUPPORTED
+    assert L.xema_op_attention(f, f, f, 1, 4, 64, 300, 384, 200, 200, f + (1 << 30), None) == X.XEMA_ERR_INVALID_ARG
+    # gemm: N not a multiple of 256
+    g = X.gemm_args(X.XEMA_BF16, f, 100, 256, f, 300, f, X.XEMA_EPI_BIAS, f + (1 << 30), X.XEMA_F16, 300)
+    assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_UNSUPPORTED
+    g = X.gemm_args(X.XEMA_BF16, f + 2, 100, 256, f, 256, f, X.XEMA_EPI_BIAS, f + (1 << 30), X.XEMA_F16, 256)
+    assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_MISALIGNED
+    # gated residual needs fp32 output
+    g = X.gemm_args(X.XEMA_F16, f, 100, 256, f, 256, f, X.XEMA_EPI_GATED_RESIDUAL, f + (1 << 30),
+                    X.XEMA_F16, 256, resid=f, ld_resid=256, gate=f)
+    assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_UNSUPPORTED
+    # LN: dim not a multiple of 256
+    assert L.xema_op_ln_modulate(f, X.XEMA_BF16, X.rowmap(4, 4, 0), 4, 300, f, f, 1800, 1e-6, f,
+                                 X.XEMA_BF16, None) == X.XEMA_ERR_UNSUPPORTED
+    # convert: overlapping buffers
+    assert L.xema_op_convert_f16(f, f + 16, 1024, None) == X.XEMA_ERR_INVALID_ARG
