@@ -17,12 +17,10 @@
 // other queries of its wave, workgroup or chunk: chunked and unchunked runs
 // agree bit for bit.
 //
-// LDS layouts.  K tile: 64 rows (keys) of HD halves; 16-byte slot c of row r
-// is stored at c ^ sK(r), sK(r) = (r & 3) | ((r >> 1) & 4), chosen so the
-// eight rows read together by eight consecutive lanes (keys 0-3 and 8-11, or
-// 4-7 and 12-15, ... of the permuted order) use eight different slots.  V^T
-// tile: HD rows (head dims) of 64 keys (128 bytes); slot c of row r at
-// c ^ (r & 7).  Tiles are filled with buffer_load ... lds, 1 KiB per wave
+// LDS layouts.  K tile: 64 rows (keys) of HD halves; V^T tile: HD rows (head
+// dims) of 64 keys (128 bytes).  The 16-byte slots of each row are XOR-
+// swizzled (swz_k, swz_v below) so that every 16-byte fragment read is free of
+// bank conflicts.  Tiles are filled with buffer_load ... lds, 1 KiB per wave
 // instruction.
 //
 // Workgroups: 4 waves = 256 queries of one (batch, head).  The grid is 1-D
@@ -65,7 +63,14 @@ __device__ __forceinline__ float pair_sum(float v) {
 __device__ __forceinline__ int kappa(int rho) {
   return ((rho >> 4) << 4) | (((rho >> 2) & 1) << 3) | (((rho >> 3) & 1) << 2) | (rho & 3);
 }
-__device__ __forceinline__ int swz_k(int r) { return (r & 3) | ((r >> 1) & 4); }
+// 16-byte slot swizzles.  The LDS has 64 four-byte banks and serves a
+// 16-byte read for 16 lanes per cycle; each group of 16 lanes reads 16
+// distinct rows (a permutation of 16 consecutive rows) at one logical slot.
+// 128-byte rows: row pairs share a 256-byte bank line, so the slot is XORed
+// with (r >> 1) & 7; 256-byte rows (K at d = 128): XOR with r & 15.
+template <int HD>
+__device__ __forceinline__ int swz_k(int r) { return HD == 64 ? (r >> 1) & 7 : r & 15; }
+__device__ __forceinline__ int swz_v(int r) { return (r >> 1) & 7; }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -124,12 +129,12 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void k_attention(AttnParams 
   for (int j = 0; j < K_INSTR; ++j) {
     const int byte = (wave + WAVES * j) * 1024 + lane * 16;
     const int row = byte / (2 * HD), ps = (byte % (2 * HD)) / 16;
-    k_off[j] = (uint32_t)((row * HD + ((ps ^ swz_k(row)) * 8)) * 2);
+    k_off[j] = (uint32_t)((row * HD + ((ps ^ swz_k<HD>(row)) * 8)) * 2);
   }
 #pragma unroll
   for (int j = 0; j < V_INSTR; ++j) {
     const int row = (wave + WAVES * j) * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ (row & 7);
+    const int c = (lane & 7) ^ swz_v(row);
     v_off[j] = (uint32_t)((row * Lp + c * 8) * 2);
   }
 
@@ -157,7 +162,7 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void k_attention(AttnParams 
 
   // fragment addressing inside the tiles
   const int krow = kappa(r32);                      // key row read by this lane
-  const int kswz = swz_k(krow);
+  const int kswz = swz_k<HD>(krow);
   const int nkv = (p.seq_len + KV - 1) / KV;
   const int tail = p.seq_len - (nkv - 1) * KV;      // valid keys in the last tile
 
@@ -241,7 +246,7 @@ __global__ __launch_bounds__(256, HD == 64 ? 2 : 1) void k_attention(AttnParams 
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const int slot16 = (kb * 4 + u * 2 + hi) ^ (vrow & 7);
+          const int slot16 = (kb * 4 + u * 2 + hi) ^ swz_v(vrow);
           const f16x8 vf = *reinterpret_cast<const f16x8*>(Vs + vrow * (KV * 2) + slot16 * 16);
 #pragma unroll
           for (int c = 0; c < 2; ++c) oacc[c][d] = mma(vf, pf[c][kb][u], oacc[c][d]);

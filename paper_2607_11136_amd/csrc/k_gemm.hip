@@ -1,14 +1,20 @@
 // C = A B^T on gfx950 bf16/fp16 MFMA, with the block's fused epilogues
 // (bias, bias + GELU-tanh, gated residual).  Steps a2, a5, a7, a8.
 //
-// Tiling: a 256 x 256 output tile per workgroup, K in steps of 64.  Four
+// Tiling: a 256 x 256 output tile per workgroup, K in steps of 32.  Four
 // waves in a 2 x 2 grid each own a 128 x 128 sub-tile held as 4 x 4
 // accumulators of v_mfma_f32_32x32x16.  Operand tiles go from HBM straight
-// into LDS with buffer_load ... lds (no VGPR staging), double-buffered; the
-// buffer descriptor of each tile covers only that tile's rows, so rows past M
-// read as zero.  Each LDS row is 64 elements (128 bytes, eight 16-byte
-// slots); slot j of row r is stored at slot j ^ (r & 7), which keeps the
-// 16-byte fragment reads of eight consecutive lanes on distinct banks.
+// into LDS with buffer_load ... lds (no VGPR staging) through a ring of four
+// stages, so up to three K-steps of loads are in flight while one is
+// consumed: a step's loads have about two steps of MFMA work to land, which
+// covers the latency of L2 misses.  The buffer descriptor of each tile covers
+// only that tile's rows, so rows past M read as zero.
+//
+// LDS layout: a stage holds 256 rows of 32 elements (64 bytes = four 16-byte
+// slots) per operand; slot j of row r is stored at slot j ^ ((r >> 2) & 3).
+// The LDS has 64 four-byte banks and serves a 16-byte read for 16 lanes per
+// cycle; those 16 lanes read 16 consecutive rows at one logical slot, and the
+// swizzle spreads them over all 64 banks.
 //
 // The MFMA takes the weight fragment as its A operand and the activation
 // fragment as its B operand, so each lane ends up holding four consecutive
@@ -18,8 +24,8 @@
 // below gives each XCD a contiguous range of tiles, walked in groups of 8
 // tile-rows, so tiles that share operand panels share an L2.
 //
-// Determinism: every output element is the sum over ascending 64-wide K
-// tiles, each reduced by the same MFMA sequence, whatever M, the row maps or
+// Determinism: every output element is the sum over ascending 32-wide K
+// steps, each reduced by the same MFMA sequence, whatever M, the row maps or
 // the tile position are; so chunked and unchunked calls agree bit for bit.
 #include "device_common.h"
 #include "kernels.h"
@@ -45,10 +51,17 @@ struct Mfma<f16> {
   }
 };
 
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int TILE_BYTES = BM * BK * 2;  // 32 KiB per operand tile
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int NS = 4;                      // LDS pipeline stages
+constexpr int OP_BYTES = BM * BK * 2;      // 16 KiB per operand per stage
+constexpr int STAGE_BYTES = 2 * OP_BYTES;
 constexpr int GROUP_M = 8;
-constexpr int BUF_FLAGS = 0x00020000;   // raw buffer, 32-bit dwords
+constexpr int NWAVES = 8;                  // 2 x 4 waves, two per SIMD
+constexpr int WN = 64;                     // output columns per wave (rows: 128)
+constexpr int NJ = WN / 32;                // 32-column MFMA blocks per wave
+constexpr int ROWS_PER_WAVE_LOAD = BM / NWAVES;  // operand rows each wave loads
+constexpr int LOADS_PER_STAGE = 2 * ROWS_PER_WAVE_LOAD / 16;  // 1 KiB loads per wave per stage
+constexpr int BUF_FLAGS = 0x00020000;      // raw buffer, 32-bit dwords
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
@@ -81,16 +94,41 @@ __device__ __forceinline__ void load4f<uint16_t>(const uint16_t* p, float v[4]) 
   v[3] = __uint_as_float(u[1] & 0xffff0000u);
 }
 
+// Workgroup barrier that lets the newest `stages_after` stages of this wave's
+// LDS-bound loads stay in flight: wait for all but the last
+// stages_after * LOADS_PER_STAGE vector-memory loads and for every LDS access,
+// then s_barrier.  (A __syncthreads() would wait for every load.)  The
+// empty asm statements keep the compiler from moving LDS accesses across.
+// s_waitcnt immediate: vmcnt[3:0] in bits 3:0 and vmcnt[5:4] in bits 15:14,
+// expcnt in bits 6:4 (7 = no wait), lgkmcnt in bits 11:8 (0 = wait for all).
+// The scheduling fences keep the MFMAs of each half-step on their side of the
+// barrier, so a wave reaches it with its MFMA queue already full.
+__device__ __forceinline__ void stage_barrier(int stages_after) {
+  static_assert(LOADS_PER_STAGE == 4, "vmcnt immediates below assume 4 loads per stage");
+  __builtin_amdgcn_sched_barrier(0);
+  if (stages_after >= 2) __builtin_amdgcn_s_waitcnt(0x0078);       // vmcnt(8)
+  else if (stages_after == 1) __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4)
+  else __builtin_amdgcn_s_waitcnt(0x0070);                         // vmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 }  // namespace
 
 // EPI: XEMA_EPI_BIAS / XEMA_EPI_BIAS_GELU (CT = bf16 or f16) or
 // XEMA_EPI_GATED_RESIDUAL (CT = float, RT = residual element type).
 template <typename T, int EPI, typename CT, typename RT>
-__global__ __launch_bounds__(256, 1) void k_gemm(GemmParams p) {
+__global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uint16_t* __restrict__ bias,
+                                                 CT* __restrict__ cout, const RT* __restrict__ resid,
+                                                 const float* __restrict__ gate) {
+  static_assert(NS == 4, "stage_barrier assumes at most two stages in flight after the next");
   typedef typename Mfma<T>::frag frag;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2][2][TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][STAGE_BYTES];
 
   const int K = p.K;
+  const int KT = K / BK;
   const int tiles_m = (int)((p.M + BM - 1) / BM);
   const int tiles_n = p.N / BN;
   const int total = tiles_m * tiles_n;
@@ -109,7 +147,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmParams p) {
   const int n0 = tn * BN;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / (BN / WN), wn = wave % (BN / WN);
 
   const T* A = reinterpret_cast<const T*>(p.a);
   const T* Bw = reinterpret_cast<const T*>(p.b);
@@ -117,68 +155,106 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmParams p) {
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * K, rows_a * K * 2);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bw + (int64_t)n0 * K, (int64_t)BN * K * 2);
 
-  // direct-to-LDS load plan: wave w fills 1 KiB chunks w*8 .. w*8+7 of each
-  // operand tile; chunk c covers rows 8c .. 8c+7, lane l writes row 8c + l/8,
-  // physical slot l%8, so it fetches logical slot (l%8) ^ (l/8).
-  const int lrow = lane >> 3;
-  const uint32_t voff = (uint32_t)(((wave * 64 + lrow) * K + (((lane & 7) ^ lrow) * 8)) * 2);
-  const uint32_t chunk_stride = (uint32_t)(8 * K * 2);
+  // Direct-to-LDS load plan: a 1 KiB wave instruction fills 16 rows; wave w
+  // fills rows 64w .. 64w+63 of each operand (4 instructions each).  Lane l
+  // writes row 16c + l/4 at physical slot l%4, so it fetches logical slot
+  // (l%4) ^ ((l >> 4) & 3).  The whole offset is in the VGPR operand, which
+  // is what the buffer range check covers (rows past M read as zero).
+  const uint32_t voff = (uint32_t)(((wave * ROWS_PER_WAVE_LOAD + (lane >> 2)) * K +
+                                    (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
+  const uint32_t chunk_stride = (uint32_t)(16 * K * 2);
 
-  auto issue = [&](int kt, int stage) {
+  // A step past the last one is issued at an offset beyond the descriptor's
+  // range: the hardware moves no data (the lanes read as zero) and the loop
+  // body stays free of branches, so its loads can be spread between MFMAs.
+  auto issue = [&](int kt) {
+    uint8_t* st = smem[kt % NS];
+    const bool valid = kt < KT;
     const uint32_t kbyte = (uint32_t)(kt * BK * 2);
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) {
-      const uint32_t so = cc * chunk_stride + kbyte;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          ra, (lds_ptr_t)(&smem[stage][0][(wave * 8 + cc) * 1024]), 16, voff, so, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rb, (lds_ptr_t)(&smem[stage][1][(wave * 8 + cc) * 1024]), 16, voff, so, 0, 0);
+    for (int c = 0; c < ROWS_PER_WAVE_LOAD / 16; ++c) {
+      const uint32_t off = valid ? voff + c * chunk_stride + kbyte : 0x80000000u;
+      const int chunk = wave * (ROWS_PER_WAVE_LOAD / 16) + c;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + chunk * 1024), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(st + OP_BYTES + chunk * 1024), 16,
+                                               off, 0, 0, 0);
     }
   };
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][NJ];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // fragment addressing: lane reads row (block + lane%32), k-slot kk*2 + lane/32
-  const int r32 = lane & 31, hi = lane >> 5, sw = lane & 7;
-  const int a_row0 = (wm * 128 + r32) * 128;  // byte offset of this lane's first A row
-  const int b_row0 = (wn * 128 + r32) * 128;
+  const int r32 = lane & 31, hi = lane >> 5, sw = (lane >> 2) & 3;
+  const int a_row0 = (wm * 128 + r32) * 64;  // byte offset of this lane's first A row
+  const int b_row0 = (wn * WN + r32) * 64;
 
-  const int KT = K / BK;
-  issue(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  frag fx[2][4], fw[2][NJ];
+  auto read_frags = [&](const uint8_t* st, int kk, frag (&x)[4], frag (&wv)[NJ]) {
+    const int so = (((kk * 2 + hi) ^ sw) * 16);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      x[i] = *reinterpret_cast<const frag*>(st + a_row0 + i * 32 * 64 + so);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      wv[j] = *reinterpret_cast<const frag*>(st + OP_BYTES + b_row0 + j * 32 * 64 + so);
+  };
+  auto mfma16 = [&](const frag (&x)[4], const frag (&wv)[NJ]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[i][j] = Mfma<T>::run(wv[j], x[i], acc[i][j]);
+  };
+
+  // prologue: steps 0 .. NS-2 in flight; step 0 must land
+  for (int s = 0; s < NS - 1; ++s) issue(s);
+  stage_barrier(NS - 2);
+  read_frags(smem[0], 0, fx[0], fw[0]);
   for (int kt = 0; kt < KT; ++kt) {
-    const int stage = kt & 1;
-    if (kt + 1 < KT) issue(kt + 1, stage ^ 1);
-    const uint8_t* As = smem[stage][0];
-    const uint8_t* Bs = smem[stage][1];
+    // The stage refilled here was consumed at step kt-1, and every wave has
+    // passed the barrier that ended step kt-1.  K-step 0 of this stage runs
+    // with the loads of step kt+NS-1 and the fragments of k-step 1 issued
+    // between its MFMAs.
+    const uint8_t* st = smem[kt % NS];
+    issue(kt + NS - 1);
+    read_frags(st, 1, fx[1], fw[1]);
+    mfma16(fx[0], fw[0]);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int so = (((kk * 2 + hi) ^ sw) * 16);
-      frag xa[4], wb[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        xa[i] = *reinterpret_cast<const frag*>(As + a_row0 + i * 32 * 128 + so);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        wb[j] = *reinterpret_cast<const frag*>(Bs + b_row0 + j * 32 * 128 + so);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = Mfma<T>::run(wb[j], xa[i], acc[i][j]);
+    for (int g = 0; g < 4 + NJ; ++g) {
+      if (g < LOADS_PER_STAGE) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                          // LDS read
+      if (g < 4 * NJ) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // MFMA
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * NJ - (4 + NJ), 0);
+    // step kt+1 must have landed; the loads of steps kt+2, kt+3 stay in flight
+    stage_barrier(NS - 2);
+    // k-step 1, with the first fragments of step kt+1 read meanwhile (after
+    // the last step this reads a stage nobody uses)
+    read_frags(smem[(kt + 1) % NS], 0, fx[0], fw[0]);
+    mfma16(fx[1], fw[1]);
+#pragma unroll
+    for (int g = 0; g < 4 + NJ; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * NJ - (4 + NJ), 0);
   }
 
   // Epilogue.  acc[i][j][r] = C[m][n] with m = m0 + wm*128 + i*32 + r32 and
-  // n = n0 + wn*128 + j*32 + 8*(r/4) + 4*hi + r%4.
+  // n = n0 + wn*128 + j*32 + 8*(r/4) + 4*hi + r%4.  Every input of a row group
+  // is loaded before any of its stores (the pointers are restrict), so the
+  // loads overlap instead of each paying a full memory latency.
+  float bv[NJ][4][4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      load4f<uint16_t>(bias + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, bv[j][q]);
   const int64_t rpb = p.c_map.rows_per_batch;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -187,45 +263,58 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmParams p) {
     const int64_t b = m / rpb;
     const int64_t within = m - b * rpb;
     const int64_t crow = b * p.c_map.batch_stride + p.c_map.row_offset + within;
-    CT* crow_ptr = reinterpret_cast<CT*>(p.c) + crow * p.ldc;
-    const RT* rrow_ptr = nullptr;
-    const float* grow = nullptr;
+    CT* crow_ptr = cout + crow * p.ldc;
+    float v[NJ][4][4];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[j][q][e] = acc[i][j][4 * q + e] + bv[j][q][e];
     if (EPI == XEMA_EPI_GATED_RESIDUAL) {
       const int64_t rrow = b * p.resid_map.batch_stride + p.resid_map.row_offset + within;
-      rrow_ptr = reinterpret_cast<const RT*>(p.resid) + rrow * p.ld_resid;
-      grow = p.gate + b * p.gate_stride;
+      const RT* rrow_ptr = resid + rrow * p.ld_resid;
+      const float* grow = gate + b * p.gate_stride;
+      float res[NJ][4][4];
+      f32x4 g[NJ][4];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = n0 + wn * WN + j * 32 + 8 * q + 4 * hi;
+          load4f<RT>(rrow_ptr + n, res[j][q]);
+          g[j][q] = *reinterpret_cast<const f32x4*>(grow + n);
+        }
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[j][q][e] = fmaf(g[j][q][e], v[j][q][e], res[j][q][e]);
+    }
+    if (EPI == XEMA_EPI_BIAS_GELU) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[j][q][e] = gelu_tanh(v[j][q][e]);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * 128 + j * 32 + 8 * q + 4 * hi;
-        float bias[4], v[4];
-        load4f<uint16_t>(p.bias + n, bias);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + bias[e];
-        if (EPI == XEMA_EPI_BIAS_GELU) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
-        }
-        if (EPI == XEMA_EPI_GATED_RESIDUAL) {
-          float res[4];
-          load4f<RT>(rrow_ptr + n, res);
-          const f32x4 g = *reinterpret_cast<const f32x4*>(grow + n);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = fmaf(g[e], v[e], res[e]);
-        }
-        store4<CT>(crow_ptr + n, v);
-      }
-    }
+      for (int q = 0; q < 4; ++q)
+        store4<CT>(crow_ptr + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, v[j][q]);
   }
 }
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   const int64_t tiles = ((p.M + BM - 1) / BM) * (p.N / BN);
   if (tiles == 0) return hipSuccess;
-  const dim3 grid((unsigned)tiles), block(256);
-#define XEMA_GEMM(T, EPI, CT, RT) hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT>), grid, block, 0, s, p)
+  const dim3 grid((unsigned)tiles), block(NWAVES * 64);
+#define XEMA_GEMM(T, EPI, CT, RT)                                                          \
+  hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT>), grid, block, 0, s, p, p.bias, (CT*)p.c,    \
+                     (const RT*)p.resid, p.gate)
   const bool h = p.dtype == XEMA_F16;
   switch (p.epilogue) {
     case XEMA_EPI_BIAS:
