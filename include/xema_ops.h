@@ -93,9 +93,11 @@ XEMA_API int xema_op_rope_table(const xema_block_cfg* cfg, const xema_request* r
  *   by xema_op_rope_table;
  *   q, k fp16 [batch, H, Lp, d]; vt fp16 [batch, H, d, Lp] (V transposed),
  *   Lp = L rounded up to XEMA_SEQ_PAD.
- * q <- RoPE(q / sqrt(mean(q^2) + qk_eps) * q_gamma), the same for k; v copied.
- * When the range ends at L, the padding tokens [L, Lp) of q, k, vt are
- * zeroed.                                                                      */
+ * k <- RoPE(k / sqrt(mean(k^2) + qk_eps) * k_gamma); q is normalised and
+ * rotated the same way with q_gamma and then multiplied by log2(e)/sqrt(d),
+ * the factor the attention softmax applies to every score (one fp16 rounding
+ * of the product); v is copied.  When the range ends at L, the padding tokens
+ * [L, Lp) of q, k, vt are zeroed.                                              */
 XEMA_API int xema_op_qk_norm_rope(const xema_block_cfg* cfg, const xema_request* req, const void* qkv,
                          int32_t tok_begin, int32_t tok_count, const void* q_gamma,
                          const void* k_gamma, const float* table, void* q, void* k,
@@ -104,7 +106,9 @@ XEMA_API int xema_op_qk_norm_rope(const xema_block_cfg* cfg, const xema_request*
 /* Step a4, joint full self-attention (no mask) for queries
  * [q_begin, q_begin + q_count) of every (batch, head), over all L keys:
  *   o[b * q_count + i][h * d + e] = sum_j softmax_j(q_i . k_j / sqrt(d)) v_j[e]
- * q, k fp16 [batch, heads, padded_len, d]; vt fp16 [batch, heads, d,
+ * given qs = q * log2(e)/sqrt(d) (as xema_op_qk_norm_rope stores it), i.e.
+ * with weights 2^(qs_i . k_j) normalised over j.
+ * qs, k fp16 [batch, heads, padded_len, d]; vt fp16 [batch, heads, d,
  * padded_len]; o fp16 [batch * q_count, heads * d].  padded_len must be a
  * multiple of XEMA_SEQ_PAD with seq_len <= padded_len, and the padding
  * columns of vt must be finite (xema_op_qk_norm_rope zeroes them).  Keys are

@@ -15,6 +15,7 @@
 // (Sec. 6.1) assigned to its slot, so runtime allocation is the table lookup
 // of Sec. 8 ("Static memory runtime").
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 
 #include "kernels.h"
@@ -150,6 +151,7 @@ static QkRopeArgs qk_args(const xema_block_cfg& cfg, const xema_request& req, co
   a.tok_begin = tok_begin; a.tok_count = tok_count;
   a.count_ext = tok_count + ((int64_t)tok_begin + tok_count == L ? (int)(Lp - L) : 0);
   a.qk_eps = cfg.qk_eps;
+  a.q_scale = (float)(1.4426950408889634 / std::sqrt((double)cfg.head_dim));
   a.geom = geom_of(cfg, req);
   return a;
 }

@@ -163,8 +163,10 @@ __global__ void k_rope_table(RopeGeom g, float theta, float2* __restrict__ table
 }
 
 // ---------------------------------------------------------------------------
-// a3: QK-RMSNorm + 3D RoPE + scatter.  Workgroup = 64 tokens of one sequence
-// x one head.  Q/K: one 16-byte slice (8 elements, 4 RoPE pairs) per item,
+// a3: QK-RMSNorm + 3D RoPE + scatter.  Queries are stored multiplied by
+// log2(e)/sqrt(d), the factor the attention softmax applies to every score,
+// so that attention can exponentiate scores with 2^x directly.  Workgroup =
+// 64 tokens of one sequence x one head.  Q/K: one 16-byte slice (8 elements, 4 RoPE pairs) per item,
 // D/8 lanes per token vector reduce the sum of squares with a butterfly.
 // V: transposed through LDS so that V^T rows of 64 tokens are stored as 128
 // contiguous bytes.  Tokens in [L, Lp) are written as zeros.
@@ -235,9 +237,11 @@ __global__ __launch_bounds__(256) void k_qk_norm_rope(QkRopeArgs a) {
         }
       }
       if (in_range) {
+        // queries carry the softmax factor log2(e)/sqrt(d) (one rounding)
+        const float f = which == 0 ? a.q_scale : 1.0f;
         f16x8 o;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (f16)v[e];
+        for (int e = 0; e < 8; ++e) o[e] = (f16)(v[e] * f);
         f16* dst = (which == 0 ? a.q : a.k) + (head_base + tok) * HD + sl * 8;
         *reinterpret_cast<f16x8*>(dst) = o;
       }

@@ -28,6 +28,7 @@ struct QkRopeArgs {
   int batch, heads, text_len, padded_len;
   int tok_begin, tok_count, count_ext;  // count_ext adds the zeroed padding tokens
   float qk_eps;
+  float q_scale;  // log2(e) / sqrt(head_dim), folded into the stored queries
   RopeGeom geom;
 };
 

@@ -85,6 +85,7 @@ def test_intermediates_in_arena_match_oracle_steps():
     for b in range(B):
         h = O.modulate(O.layer_norm(x[b], s.ln_eps), m[b, :D], m[b, D:2 * D])
         qr, kr, vr = O.qkv_heads(h, w, H, d, coords, s.rope_dims, s.rope_theta, s.qk_eps)
+        qr = qr * (np.log2(np.e) / np.sqrt(d))   # the softmax factor the stored queries carry
         # bf16 h and fp16 qkv / Q / K / V roundings on the GPU side
         for got, ref in ((q[b, :, :L].transpose(1, 0, 2), qr), (k[b, :, :L].transpose(1, 0, 2), kr),
                          (vt[b, :, :, :L].transpose(2, 0, 1), vr)):

@@ -13,6 +13,8 @@ from gpu_util import DEV, bf16_dev, cfg_of, req_of
 
 pytestmark = pytest.mark.gpu
 
+LOG2E = 1.4426950408889634
+
 
 def _rng(seed):
     return np.random.default_rng(seed)
@@ -204,6 +206,8 @@ def test_qk_norm_rope_matches_oracle(head_dim, rope_dims, grid, text_len):
         z = q64[:, :, which * D:(which + 1) * D].reshape(B, L, H, head_dim)
         ref = np.stack([O.rope_rotate(O.rms_norm(z[b], W.bf16_bits_to_f64(gam[gname]), 1e-6), ang)
                         for b in range(B)])           # [B, L, H, d]
+        if which == 0:   # stored queries carry the softmax factor log2(e)/sqrt(d)
+            ref = ref * (LOG2E / np.sqrt(head_dim))
         got = out.float().cpu().numpy()
         _check_close(got[:, :, :L].transpose(0, 2, 1, 3), ref, 2.0 ** -10, 1e-4, f"qk_norm_rope {gname}")
         assert np.all(got[:, :, L:] == 0)
@@ -220,13 +224,15 @@ def test_attention_matches_oracle(head_dim, L, q0, qn, scale):
     B, H = 2, 3
     Lp = X.padded_len(L)
     g = _rng(L + head_dim)
-    q = _f16(g.standard_normal((B, H, L, head_dim)) * scale)
+    # the op takes queries pre-multiplied by log2(e)/sqrt(d): weights 2^(qs . k)
+    qs = _f16(g.standard_normal((B, H, L, head_dim)) * (scale * LOG2E / np.sqrt(head_dim)))
     k = _f16(g.standard_normal((B, H, L, head_dim)) * scale)
     v = _f16(g.standard_normal((B, H, L, head_dim)))
+    q = qs.astype(np.float64) * (np.sqrt(head_dim) / LOG2E)
     qd = torch.zeros((B, H, Lp, head_dim), dtype=torch.float16, device=DEV)
     kd = torch.zeros_like(qd)
     vtd = torch.zeros((B, H, head_dim, Lp), dtype=torch.float16, device=DEV)
-    qd[:, :, :L] = torch.from_numpy(q).to(DEV)
+    qd[:, :, :L] = torch.from_numpy(qs).to(DEV)
     kd[:, :, :L] = torch.from_numpy(k).to(DEV)
     vtd[:, :, :, :L] = torch.from_numpy(np.ascontiguousarray(v.transpose(0, 1, 3, 2))).to(DEV)
     o = torch.empty((B * qn, H * head_dim), dtype=torch.float16, device=DEV)
@@ -236,7 +242,7 @@ def test_attention_matches_oracle(head_dim, L, q0, qn, scale):
     ref = np.empty((B, qn, H, head_dim))
     for b in range(B):
         for h in range(H):
-            ref[b, :, h] = O.attention(q[b, h, q0:q0 + qn].astype(np.float64), k[b, h].astype(np.float64),
+            ref[b, :, h] = O.attention(q[b, h, q0:q0 + qn], k[b, h].astype(np.float64),
                                        v[b, h].astype(np.float64))
     _check_close(got, ref, 2.0 ** -9, 2e-3, f"attention d={head_dim} L={L} q=[{q0},{q0 + qn}) x{scale}")
 
