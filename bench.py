@@ -94,12 +94,49 @@ def bench_gpu(args, shape):
     torch.cuda.synchronize()
     attn_ms = a0.elapsed_time(a1) / n_attn
     print(f"[bench] attention kernel: {attn_ms:.3f} ms per launch", file=sys.stderr, flush=True)
+    if args.copy_bytes > 0:
+        # a plain device-to-device copy of known size, so that HBM byte counters
+        # read under a profiler can be scaled to bytes
+        src = torch.ones(args.copy_bytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copied {args.copy_bytes} bytes x 3", file=sys.stderr, flush=True)
     return {
         "ms": ms,
         "attn_ms": attn_ms,
         "plan": plan,
         "device_peak_bytes": int(torch.cuda.max_memory_allocated()),
     }
+
+
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attention_video_hbm_traffic.md")
+TRAFFIC_SOURCES = ("paper_2607_11136_amd/csrc/k_attention.hip", "paper_2607_11136_amd/csrc/device_common.h",
+                   "paper_2607_11136_amd/csrc/kernels.h")
+
+
+def attention_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when it is missing or was taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_RECORD) as f:
+            line = next(l for l in f if l.startswith("record: "))
+        rec = json.loads(line[len("record: "):])
+    except (OSError, StopIteration, ValueError):
+        return None
+    if rec.get("source_sha256") != attention_source_digest():
+        return None
+    return int(rec["fetch_bytes"] + rec["write_bytes"])
 
 
 def cpu_baseline(shape, n_rows):
@@ -145,7 +182,14 @@ def main():
     ap.add_argument("--budget", type=int, default=2 << 30, help="activation budget (arena bytes)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="also run a plain device copy of this size (calibrates HBM byte counters)")
+    ap.add_argument("--print-digest", action="store_true",
+                    help="print the digest of the attention kernel sources and exit")
     args = ap.parse_args()
+    if args.print_digest:
+        print(attention_source_digest())
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the block forward is measured on a single MI355X "
               "(multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
@@ -191,7 +235,7 @@ def main():
             "frac": round(attn_tflops / PEAK_TFLOPS, 4),
             "ms_per_launch": round(g["attn_ms"], 4),
             "flops_per_launch": af,
-            "traffic": None,
+            "traffic": measured_traffic(),
         },
     }
     if not args.no_cpu_baseline:
