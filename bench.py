@@ -227,7 +227,7 @@ def main():
             "arena_bytes": plan.workspace_bytes, "device_peak_bytes": g["device_peak_bytes"],
         },
         "roofline": {
-            "kernel": "k_attention<64> (joint attention, all 17776 queries x 17776 keys x 48 heads)",
+            "kernel": "k_attention_lazy<64> (joint attention, all 17776 queries x 17776 keys x 48 heads)",
             "bound": "mfma",
             "achieved": round(attn_tflops, 2),
             "peak": PEAK_TFLOPS,
