@@ -46,14 +46,14 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// GELU, tanh form: 0.5 u (1 + tanh(a (u + 0.044715 u^3))), a = sqrt(2/pi),
-// written with tanh(z) = 1 - 2 / (exp(2z) + 1).
+// GELU, tanh form: 0.5 u (1 + tanh(a (u + 0.044715 u^3))), a = sqrt(2/pi).
+// Since 0.5 (1 + tanh(z)) = 1 / (1 + e^(-2z)), this is u / (1 + 2^(-2 z log2 e)),
+// taken with the hardware exp2 and reciprocal (about 1 ulp each).  Large |u|
+// gives 2^(+inf) -> 1/inf = 0 or 2^(-inf) -> 1/1 = 1, so no NaN appears.
 __device__ __forceinline__ float gelu_tanh(float u) {
-  const float a = 0.7978845608028654f;
-  const float z = a * fmaf(0.044715f * u, u * u, u);
-  const float e = __expf(2.0f * z);
-  const float t = 1.0f - 2.0f / (e + 1.0f);
-  return 0.5f * u * (1.0f + t);
+  const float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 a log2(e)
+  const float e = __builtin_amdgcn_exp2f(c * fmaf(0.044715f * u, u * u, u));
+  return u * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 }  // namespace xema

@@ -24,7 +24,8 @@
 //     ring so one group's softmax overlaps the other's MFMAs;
 //   k_attention_lazy (used at d = 64): two column blocks per wave (half the
 //     LDS reads per score), a 2-stage ring, and a trigger on the tile max
-//     exceeding the reference by TAU = 8 (v_max3 reductions).
+//     exceeding the reference by TAU = 8 (v_max3 reductions), which leaves the
+//     exponentials out of the branch; row sums by v_dot2 as above.
 // Measured on the workloads' own Q/K/V, each is the faster one at its width.
 //
 // Keys are visited in one fixed ascending order of 64-key tiles, and every
@@ -112,9 +113,9 @@ __device__ __forceinline__ float exp_pack(const f32x16& s0, const f32x16& s1, fl
         const float x0 = SHIFT ? sv[8 * u + e] - shift : sv[8 * u + e];
         const float x1 = SHIFT ? sv[8 * u + e + 1] - shift : sv[8 * u + e + 1];
         const f16x2 h = {(f16)fast_exp2(x0), (f16)fast_exp2(x1)};
+        acc = __builtin_amdgcn_fdot2(h, one, acc, false);
         pf[kb][u][e] = h[0];
         pf[kb][u][e + 1] = h[1];
-        acc = __builtin_amdgcn_fdot2(h, one, acc, false);
       }
   return acc;
 }
@@ -228,6 +229,45 @@ __device__ __forceinline__ void tile_softmax(const f32x16 (&s)[2][QB], bool firs
   }
 #pragma unroll
   for (int c = 0; c < QB; ++c) st.lrow[c] += lsp[c];
+}
+
+// Online softmax of one tile for k_attention_lazy: scores arrive unshifted;
+// a column grows when its tile max exceeds mrow by more than TAU (and on the
+// first tile), and only then do mrow move and O and the row sum get rescaled.
+// P = 2^(s - mrow) <= 2^TAU; the row sum is the v_dot2 sum of the packed P.
+template <int HD, int QB>
+__device__ __forceinline__ void tile_softmax_maxtrig(const f32x16 (&s)[2][QB], bool first,
+                                                     WaveState<HD, QB>& st,
+                                                     f16x8 (&pf)[QB][2][2]) {
+  float mxs[QB];
+  bool grow_any = first;
+#pragma unroll
+  for (int c = 0; c < QB; ++c) {
+    float mx = s[0][c][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][c][r]);
+    mxs[c] = pair_max(mx);
+    grow_any |= mxs[c] - st.mrow[c] > TAU;
+  }
+  if (__builtin_amdgcn_ballot_w64(grow_any)) {
+#pragma unroll
+    for (int c = 0; c < QB; ++c) {
+      const bool grow = first || mxs[c] - st.mrow[c] > TAU;
+      const float alpha = first ? 0.f : (grow ? fast_exp2(st.mrow[c] - mxs[c]) : 1.f);
+      if (grow) st.mrow[c] = mxs[c];
+      st.lrow[c] *= alpha;
+#pragma unroll
+      for (int d = 0; d < HD / 32; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st.oacc[c][d][r] *= alpha;
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < QB; ++c) {
+    st.lrow[c] += exp_pack<true>(s[0][c], s[1][c], st.mrow[c], pf[c]);
+  }
 }
 
 // O^T += V^T P^T
@@ -406,6 +446,32 @@ void k_attention(AttnParams p) {
   }
 }
 
+// One key tile of k_attention_lazy (tile kv in stage kv & 1; the next tile
+// is loaded into the other stage meanwhile).  LAST masks the keys at or past
+// `tail` and loads nothing.
+template <int HD, int QB, int NW, int K_INSTR, int V_INSTR, bool LAST>
+__device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int kv, int tail,
+                                          __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                          const uint32_t (&k_off)[K_INSTR],
+                                          const uint32_t (&v_off)[V_INSTR], int wave,
+                                          const f16x8 (&qf)[QB][HD / 16], int krow, int kswz,
+                                          int r32, int hi, WaveState<HD, QB>& st) {
+  constexpr int K_BYTES = KV * HD * 2;
+  const int stage = kv & 1;
+  if (!LAST)
+    issue_kv<K_INSTR, V_INSTR, K_BYTES, NW>(rk, rv, k_off, v_off, smem[stage ^ 1], wave,
+                                            (uint32_t)((kv + 1) * KV * HD * 2),
+                                            (uint32_t)((kv + 1) * KV * 2));
+  f32x16 s[2][QB];
+  f16x8 pf[QB][2][2];
+  tile_scores<HD, QB>(smem[stage], qf, st.minit, krow, kswz, hi, s);
+  if (LAST && tail < KV) mask_tail<QB>(s, tail, hi);
+  tile_softmax_maxtrig<HD, QB>(s, kv == 0, st, pf);
+  tile_pv<HD, QB>(smem[stage] + K_BYTES, pf, r32, hi, st.oacc);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
 // Variant for narrow heads (d = 64): no group offset, two query column
 // blocks per wave (halving the LDS reads per score), a two-stage ring, and a
 // lazy max that moves when a tile's max exceeds the one in use by more than
@@ -473,19 +539,17 @@ __global__ __launch_bounds__(NW * 64) void k_attention_lazy(AttnParams p) {
       qf[c][kk] = *reinterpret_cast<const f16x8*>(Qh + (int64_t)q * HD + kk * 16 + hi * 8);
   }
 
-  f32x16 oacc[QB][NDB];
+  WaveState<HD, QB> st;
 #pragma unroll
-  for (int c = 0; c < QB; ++c)
+  for (int c = 0; c < QB; ++c) {
+    st.mrow[c] = 0.f;
+    st.lrow[c] = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) st.minit[c][r] = 0.f;
 #pragma unroll
     for (int d = 0; d < NDB; ++d)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[c][d][r] = 0.f;
-  // mrow: the max in use (log2 units); lrow: this lane's share of the row sum
-  float mrow[QB], lrow[QB];
-#pragma unroll
-  for (int c = 0; c < QB; ++c) {
-    mrow[c] = 0.f;
-    lrow[c] = 0.f;
+      for (int r = 0; r < 16; ++r) st.oacc[c][d][r] = 0.f;
   }
 
   // fragment addressing inside the tiles
@@ -497,110 +561,18 @@ __global__ __launch_bounds__(NW * 64) void k_attention_lazy(AttnParams p) {
   issue_kv<K_INSTR, V_INSTR, K_BYTES, NW>(rk, rv, k_off, v_off, smem[0], wave, 0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  for (int kv = 0; kv < nkv; ++kv) {
-    const int stage = kv & 1;
-    if (kv + 1 < nkv)
-      issue_kv<K_INSTR, V_INSTR, K_BYTES, NW>(rk, rv, k_off, v_off, smem[stage ^ 1], wave,
-                                              (uint32_t)((kv + 1) * KV * HD * 2),
-                                              (uint32_t)((kv + 1) * KV * 2));
-    const uint8_t* Ks = smem[stage];
-    const uint8_t* Vs = smem[stage] + K_BYTES;
-
-    // S^T = K Q^T for two 32-key blocks x QB query columns
-    f32x16 s[2][QB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int row = kb * 32 + krow;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        const int slot16 = (kk * 2 + hi) ^ kswz;
-        const f16x8 kf = *reinterpret_cast<const f16x8*>(Ks + row * (HD * 2) + slot16 * 16);
-#pragma unroll
-        for (int c = 0; c < QB; ++c) s[kb][c] = mma(kf, qf[c][kk], kk == 0 ? f32x16{} : s[kb][c]);
-      }
-    }
-    if (kv == nkv - 1 && tail < KV) {
-      // lane's score r of block kb is key kb*32 + 16*(r>>3) + 8*hi + (r&7)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kb * 32 + 16 * (r >> 3) + 8 * hi + (r & 7);
-          if (key >= tail) {
-#pragma unroll
-            for (int c = 0; c < QB; ++c) s[kb][c][r] = -INFINITY;
-          }
-        }
-    }
-    // Online softmax per query column with a lazy max.  A column "grows" when
-    // its tile max exceeds mrow by more than TAU (and on the first tile, to
-    // set mrow); only then does mrow move and O get rescaled.  The wave takes
-    // the rescaling path when any lane grows; the other lanes keep their mrow
-    // and multiply by exactly 1.0.
-    f16x8 pf[QB][2][2];  // [column][key block][16-key half]
-    float mxs[QB];
-    bool grow_any = kv == 0;
-#pragma unroll
-    for (int c = 0; c < QB; ++c) {
-      float mx = s[0][c][0];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][c][r]);
-      mxs[c] = pair_max(mx);
-      grow_any |= mxs[c] - mrow[c] > TAU;
-    }
-    if (__builtin_amdgcn_ballot_w64(grow_any)) {
-#pragma unroll
-      for (int c = 0; c < QB; ++c) {
-        const bool grow = kv == 0 || mxs[c] - mrow[c] > TAU;
-        const float alpha = kv == 0 ? 0.f : (grow ? fast_exp2(mrow[c] - mxs[c]) : 1.f);
-        if (grow) mrow[c] = mxs[c];
-        lrow[c] *= alpha;
-#pragma unroll
-        for (int d = 0; d < NDB; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[c][d][r] *= alpha;
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < QB; ++c) {
-      float ls = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float pv = fast_exp2(s[kb][c][8 * u + e] - mrow[c]);
-            ls += pv;
-            pf[c][kb][u][e] = (f16)pv;
-          }
-      lrow[c] += ls;
-    }
-    // O^T += V^T P^T
-#pragma unroll
-    for (int d = 0; d < NDB; ++d) {
-      const int vrow = d * 32 + r32;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int slot16 = (kb * 4 + u * 2 + hi) ^ swz_v(vrow);
-          const f16x8 vf = *reinterpret_cast<const f16x8*>(Vs + vrow * (KV * 2) + slot16 * 16);
-#pragma unroll
-          for (int c = 0; c < QB; ++c) oacc[c][d] = mma(vf, pf[c][kb][u], oacc[c][d]);
-        }
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-  }
+  // the last tile, the only one with masked keys, is peeled off the loop
+  for (int kv = 0; kv < nkv - 1; ++kv)
+    lazy_iter<HD, QB, NW, K_INSTR, V_INSTR, false>(smem, kv, 0, rk, rv, k_off, v_off, wave, qf, krow,
+                                                   kswz, r32, hi, st);
+  lazy_iter<HD, QB, NW, K_INSTR, V_INSTR, true>(smem, nkv - 1, tail, rk, rv, k_off, v_off, wave, qf,
+                                                krow, kswz, r32, hi, st);
 
   // normalise and store O[b * q_count + (q - q_begin)][h*HD + dim]
 #pragma unroll
   for (int c = 0; c < QB; ++c) {
     const int q = q_first + c * 32 + r32;
-    const float inv = 1.0f / pair_sum(lrow[c]);
+    const float inv = 1.0f / pair_sum(st.lrow[c]);
     if (q >= p.q_begin + p.q_count) continue;
     f16* orow = p.o + ((int64_t)b * p.q_count + (q - p.q_begin)) * ((int64_t)p.heads * HD) +
                 (int64_t)h * HD;
@@ -610,7 +582,7 @@ __global__ __launch_bounds__(NW * 64) void k_attention_lazy(AttnParams p) {
       for (int g = 0; g < 4; ++g) {
         f16x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (f16)(oacc[c][d][4 * g + e] * inv);
+        for (int e = 0; e < 4; ++e) o[e] = (f16)(st.oacc[c][d][4 * g + e] * inv);
         *reinterpret_cast<f16x4*>(orow + d * 32 + 8 * g + 4 * hi) = o;
       }
   }

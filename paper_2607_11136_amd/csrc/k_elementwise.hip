@@ -175,73 +175,102 @@ template <int HD>
 __global__ __launch_bounds__(256) void k_qk_norm_rope(QkRopeArgs a) {
   constexpr int SL = HD / 8;               // 16-byte slices per head vector
   constexpr int TOK = 64;
+  static_assert(256 % SL == 0, "a thread keeps one slice");
   __shared__ f16 vs[TOK][HD + 8];
+  __shared__ int tpos[TOK][3];             // (t, y, w) of each visual token, -1 for text
   const int h = blockIdx.y, b = blockIdx.z;
   const int t0 = blockIdx.x * TOK;         // offset inside [0, count_ext)
   const int tid = threadIdx.x;
   const int64_t D = (int64_t)a.heads * HD;
   const int64_t head_base = ((int64_t)b * a.heads + h) * a.padded_len;
 
+  if (tid < TOK) {
+    const int vi = a.tok_begin + t0 + tid - a.text_len;
+    const int gw = a.geom.grid[2], hw = a.geom.grid[1] * gw;
+    tpos[tid][0] = vi < 0 ? -1 : vi / hw;
+    tpos[tid][1] = vi < 0 ? 0 : (vi % hw) / gw;
+    tpos[tid][2] = vi < 0 ? 0 : vi % gw;
+  }
+  // This thread's slice never changes: find the RoPE axis, the pair index in
+  // that axis and the axis' table base for each of its 4 pairs (axis -1: the
+  // pair lies past the rotated dims).
+  const int sl = tid % SL;
+  int pax[4], pidx[4], pnp[4], pbase[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int pair = sl * 4 + e;
+    int pair0 = 0, tbase = 0;
+    pax[e] = -1; pidx[e] = 0; pnp[e] = 0; pbase[e] = 0;
+#pragma unroll
+    for (int ax = 0; ax < 3; ++ax) {
+      const int np = a.geom.dims[ax] / 2;
+      if (pax[e] < 0 && pair >= pair0 && pair < pair0 + np) {
+        pax[e] = ax; pidx[e] = pair - pair0; pnp[e] = np; pbase[e] = tbase;
+      }
+      pair0 += np;
+      tbase += a.geom.grid[ax] * np;
+    }
+  }
+  float gq[8], gk[8];
+  {
+    const u32x4 vq = *reinterpret_cast<const u32x4*>(a.q_gamma + sl * 8);
+    const u32x4 vk = *reinterpret_cast<const u32x4*>(a.k_gamma + sl * 8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      gq[2 * e] = __uint_as_float(vq[e] << 16);
+      gq[2 * e + 1] = __uint_as_float(vq[e] & 0xffff0000u);
+      gk[2 * e] = __uint_as_float(vk[e] << 16);
+      gk[2 * e + 1] = __uint_as_float(vk[e] & 0xffff0000u);
+    }
+  }
+  __syncthreads();
+
   // Q and K
-  for (int item = tid; item < TOK * SL; item += 256) {
-    const int ti = item / SL, sl = item % SL;
+  for (int ti = tid / SL; ti < TOK; ti += 256 / SL) {
     const int i = t0 + ti;                 // index inside the range
     const int tok = a.tok_begin + i;       // position in the sequence
     const bool in_range = i < a.count_ext;
     const bool real = i < a.tok_count;     // a token with input (tok < L)
+    f16x8 u[2] = {};
+    if (real) {
+      const f16* row = a.qkv + ((int64_t)b * a.tok_count + i) * 3 * D + (int64_t)h * HD + sl * 8;
+      u[0] = *reinterpret_cast<const f16x8*>(row);
+      u[1] = *reinterpret_cast<const f16x8*>(row + D);
+    }
+    float2 cs[4];
+    const int tp = tpos[ti][0];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      cs[e] = make_float2(1.f, 0.f);
+      if (real && tp >= 0 && pax[e] >= 0) {
+        const int pos = tpos[ti][pax[e]];
+        cs[e] = a.table[pbase[e] + pos * pnp[e] + pidx[e]];
+      }
+    }
 #pragma unroll
     for (int which = 0; which < 2; ++which) {
       float v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      if (real) {
-        const f16x8 u = *reinterpret_cast<const f16x8*>(
-            a.qkv + ((int64_t)b * a.tok_count + i) * 3 * D + which * D + (int64_t)h * HD + sl * 8);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = (float)u[e];
-      }
+      for (int e = 0; e < 8; ++e) v[e] = (float)u[which][e];
       float ss = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) ss = fmaf(v[e], v[e], ss);
 #pragma unroll
       for (int o = SL / 2; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
-      const float r = 1.0f / sqrtf(ss / (float)HD + a.qk_eps);
-      const uint16_t* gam = which == 0 ? a.q_gamma : a.k_gamma;
-      const u32x4 gv = *reinterpret_cast<const u32x4*>(gam + sl * 8);
+      // 1/sqrt(mean + eps) with the hardware reciprocal square root (1 ulp)
+      const float r = __builtin_amdgcn_rsqf(ss * (1.0f / (float)HD) + a.qk_eps);
+      const float* g = which == 0 ? gq : gk;
+      // queries also carry the softmax factor log2(e)/sqrt(d), applied after
+      // the rotation with the normalisation, so there is one rounding
+      const float f = which == 0 ? a.q_scale : 1.0f;
+      f16x8 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        v[2 * e] *= r * __uint_as_float(gv[e] << 16);
-        v[2 * e + 1] *= r * __uint_as_float(gv[e] & 0xffff0000u);
-      }
-      // RoPE on the 4 pairs of this slice (text tokens and tail dims unrotated)
-      if (real && tok >= a.text_len) {
-        const int vi = tok - a.text_len;
-        const int hw = a.geom.grid[1] * a.geom.grid[2];
-        const int pos[3] = {vi / hw, (vi % hw) / a.geom.grid[2], vi % a.geom.grid[2]};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int pair = sl * 4 + e;
-          int pair0 = 0, tbase = 0;
-#pragma unroll
-          for (int ax = 0; ax < 3; ++ax) {
-            const int np = a.geom.dims[ax] / 2;
-            if (pair >= pair0 && pair < pair0 + np) {
-              const float2 cs = a.table[tbase + pos[ax] * np + (pair - pair0)];
-              const float u0 = v[2 * e], u1 = v[2 * e + 1];
-              v[2 * e] = fmaf(u0, cs.x, -u1 * cs.y);
-              v[2 * e + 1] = fmaf(u0, cs.y, u1 * cs.x);
-            }
-            pair0 += np;
-            tbase += a.geom.grid[ax] * np;
-          }
-        }
+        const float u0 = v[2 * e] * r * g[2 * e], u1 = v[2 * e + 1] * r * g[2 * e + 1];
+        o[2 * e] = (f16)(fmaf(u0, cs[e].x, -u1 * cs[e].y) * f);
+        o[2 * e + 1] = (f16)(fmaf(u0, cs[e].y, u1 * cs[e].x) * f);
       }
       if (in_range) {
-        // queries carry the softmax factor log2(e)/sqrt(d) (one rounding)
-        const float f = which == 0 ? a.q_scale : 1.0f;
-        f16x8 o;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (f16)(v[e] * f);
         f16* dst = (which == 0 ? a.q : a.k) + (head_base + tok) * HD + sl * 8;
         *reinterpret_cast<f16x8*>(dst) = o;
       }

@@ -1,9 +1,9 @@
 // C = A B^T on gfx950 bf16/fp16 MFMA, with the block's fused epilogues
 // (bias, bias + GELU-tanh, gated residual).  Steps a2, a5, a7, a8.
 //
-// Tiling: a 256 x 256 output tile per workgroup, K in steps of 32.  Four
-// waves in a 2 x 2 grid each own a 128 x 128 sub-tile held as 4 x 4
-// accumulators of v_mfma_f32_32x32x16.  Operand tiles go from HBM straight
+// Tiling: a 256 x 256 output tile per workgroup, K in steps of 32.  Eight
+// waves (two per SIMD) in a 2 x 4 grid each own a 128 x 64 sub-tile held as
+// 4 x 2 accumulators of v_mfma_f32_32x32x16.  Operand tiles go from HBM straight
 // into LDS with buffer_load ... lds (no VGPR staging) through a ring of four
 // stages, so up to three K-steps of loads are in flight while one is
 // consumed: a step's loads have about two steps of MFMA work to land, which
@@ -56,8 +56,11 @@ constexpr int NS = 4;                      // LDS pipeline stages
 constexpr int OP_BYTES = BM * BK * 2;      // 16 KiB per operand per stage
 constexpr int STAGE_BYTES = 2 * OP_BYTES;
 constexpr int GROUP_M = 8;
-constexpr int NWAVES = 8;                  // 2 x 4 waves, two per SIMD
-constexpr int WN = 64;                     // output columns per wave (rows: 128)
+#ifndef XEMA_GEMM_NWAVES
+#define XEMA_GEMM_NWAVES 8
+#endif
+constexpr int NWAVES = XEMA_GEMM_NWAVES;   // 8: 2 x 4 waves, two per SIMD; 4: 2 x 2, one per SIMD
+constexpr int WN = BN * 2 / NWAVES;        // output columns per wave (rows: 128)
 constexpr int NJ = WN / 32;                // 32-column MFMA blocks per wave
 constexpr int ROWS_PER_WAVE_LOAD = BM / NWAVES;  // operand rows each wave loads
 constexpr int LOADS_PER_STAGE = 2 * ROWS_PER_WAVE_LOAD / 16;  // 1 KiB loads per wave per stage
@@ -103,12 +106,14 @@ __device__ __forceinline__ void load4f<uint16_t>(const uint16_t* p, float v[4]) 
 // expcnt in bits 6:4 (7 = no wait), lgkmcnt in bits 11:8 (0 = wait for all).
 // The scheduling fences keep the MFMAs of each half-step on their side of the
 // barrier, so a wave reaches it with its MFMA queue already full.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+
 __device__ __forceinline__ void stage_barrier(int stages_after) {
-  static_assert(LOADS_PER_STAGE == 4, "vmcnt immediates below assume 4 loads per stage");
+  static_assert(2 * LOADS_PER_STAGE < 64, "vmcnt range");
   __builtin_amdgcn_sched_barrier(0);
-  if (stages_after >= 2) __builtin_amdgcn_s_waitcnt(0x0078);       // vmcnt(8)
-  else if (stages_after == 1) __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4)
-  else __builtin_amdgcn_s_waitcnt(0x0070);                         // vmcnt(0)
+  if (stages_after >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS_PER_STAGE));
+  else if (stages_after == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS_PER_STAGE));
+  else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
