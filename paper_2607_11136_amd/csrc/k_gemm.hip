@@ -1,20 +1,27 @@
 // C = A B^T on gfx950 bf16/fp16 MFMA, with the block's fused epilogues
 // (bias, bias + GELU-tanh, gated residual).  Steps a2, a5, a7, a8.
 //
-// Tiling: a 256 x 256 output tile per workgroup, K in steps of 32.  Eight
-// waves (two per SIMD) in a 2 x 4 grid each own a 128 x 64 sub-tile held as
-// 4 x 2 accumulators of v_mfma_f32_32x32x16.  Operand tiles go from HBM straight
-// into LDS with buffer_load ... lds (no VGPR staging) through a ring of four
-// stages, so up to three K-steps of loads are in flight while one is
-// consumed: a step's loads have about two steps of MFMA work to land, which
-// covers the latency of L2 misses.  The buffer descriptor of each tile covers
-// only that tile's rows, so rows past M read as zero.
+// Tiling: a BM x 256 output tile per workgroup (BM = 256 or 128), K in steps
+// of 32.  Eight waves (two per SIMD) in a 2 x 4 grid each own a (BM/2) x 64
+// sub-tile held as (BM/64) x 2 accumulators of v_mfma_f32_32x32x16.  Operand
+// tiles go from HBM straight into LDS with buffer_load ... lds (no VGPR
+// staging) through a ring of four stages, so up to three K-steps of loads are
+// in flight while one is consumed: a step's loads have about two steps of
+// MFMA work to land, which covers the latency of L2 misses.  The buffer
+// descriptor of each tile covers only that tile's rows, so rows past M read
+// as zero.
 //
-// LDS layout: a stage holds 256 rows of 32 elements (64 bytes = four 16-byte
-// slots) per operand; slot j of row r is stored at slot j ^ ((r >> 2) & 3).
-// The LDS has 64 four-byte banks and serves a 16-byte read for 16 lanes per
-// cycle; those 16 lanes read 16 consecutive rows at one logical slot, and the
-// swizzle spreads them over all 64 banks.
+// A launch covers a range of rows.  The launcher splits the rows between a
+// 256-row-tile launch and a 128-row-tile launch so that the last wave of
+// workgroups over the 256 CUs is as full as possible (e.g. 17776 x 3072 is
+// 840 tiles of 256 x 256 = 3.3 waves; 64 tile-rows of 256 plus 11 of 128 fill
+// 3 waves and half a wave of half-size tiles).
+//
+// LDS layout: a stage holds BM rows of A and 256 rows of B, 32 elements (64
+// bytes = four 16-byte slots) each; slot j of row r is stored at slot
+// j ^ ((r >> 2) & 3).  The LDS has 64 four-byte banks and serves a 16-byte
+// read for 16 lanes per cycle; those 16 lanes read 16 consecutive rows at
+// one logical slot, and the swizzle spreads them over all 64 banks.
 //
 // The MFMA takes the weight fragment as its A operand and the activation
 // fragment as its B operand, so each lane ends up holding four consecutive
@@ -25,8 +32,9 @@
 // tile-rows, so tiles that share operand panels share an L2.
 //
 // Determinism: every output element is the sum over ascending 32-wide K
-// steps, each reduced by the same MFMA sequence, whatever M, the row maps or
-// the tile position are; so chunked and unchunked calls agree bit for bit.
+// steps, each reduced by the same MFMA sequence, whatever M, BM, the row maps
+// or the tile position are; so chunked and unchunked calls, and either tile
+// height, agree bit for bit.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -51,19 +59,13 @@ struct Mfma<f16> {
   }
 };
 
-constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int BN = 256, BK = 32;
 constexpr int NS = 4;                      // LDS pipeline stages
-constexpr int OP_BYTES = BM * BK * 2;      // 16 KiB per operand per stage
-constexpr int STAGE_BYTES = 2 * OP_BYTES;
+constexpr int B_BYTES = BN * BK * 2;       // 16 KiB of B per stage
 constexpr int GROUP_M = 8;
-#ifndef XEMA_GEMM_NWAVES
-#define XEMA_GEMM_NWAVES 8
-#endif
-constexpr int NWAVES = XEMA_GEMM_NWAVES;   // 8: 2 x 4 waves, two per SIMD; 4: 2 x 2, one per SIMD
-constexpr int WN = BN * 2 / NWAVES;        // output columns per wave (rows: 128)
+constexpr int NWAVES = 8;                  // 2 x 4 waves, two per SIMD
+constexpr int WN = 64;                     // output columns per wave
 constexpr int NJ = WN / 32;                // 32-column MFMA blocks per wave
-constexpr int ROWS_PER_WAVE_LOAD = BM / NWAVES;  // operand rows each wave loads
-constexpr int LOADS_PER_STAGE = 2 * ROWS_PER_WAVE_LOAD / 16;  // 1 KiB loads per wave per stage
 constexpr int BUF_FLAGS = 0x00020000;      // raw buffer, 32-bit dwords
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
@@ -108,6 +110,7 @@ __device__ __forceinline__ void load4f<uint16_t>(const uint16_t* p, float v[4]) 
 // barrier, so a wave reaches it with its MFMA queue already full.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
+template <int LOADS_PER_STAGE>
 __device__ __forceinline__ void stage_barrier(int stages_after) {
   static_assert(2 * LOADS_PER_STAGE < 64, "vmcnt range");
   __builtin_amdgcn_sched_barrier(0);
@@ -123,18 +126,26 @@ __device__ __forceinline__ void stage_barrier(int stages_after) {
 }  // namespace
 
 // EPI: XEMA_EPI_BIAS / XEMA_EPI_BIAS_GELU (CT = bf16 or f16) or
-// XEMA_EPI_GATED_RESIDUAL (CT = float, RT = residual element type).
-template <typename T, int EPI, typename CT, typename RT>
-__global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uint16_t* __restrict__ bias,
+// XEMA_EPI_GATED_RESIDUAL (CT = float, RT = residual element type).  Rows
+// [m_begin, M) in tiles of BM rows.
+template <typename T, int EPI, typename CT, typename RT, int BM>
+__global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m_begin,
+                                                 const uint16_t* __restrict__ bias,
                                                  CT* __restrict__ cout, const RT* __restrict__ resid,
                                                  const float* __restrict__ gate) {
   static_assert(NS == 4, "stage_barrier assumes at most two stages in flight after the next");
+  static_assert(BM == 256 || BM == 128, "tile heights");
+  constexpr int MI = BM / 64;                         // 32-row MFMA blocks per wave
+  constexpr int A_BYTES = BM * BK * 2;
+  constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  constexpr int A_LOADS = BM / 128, B_LOADS = BN / 128;  // 1 KiB loads per wave per stage
+  constexpr int LPS = A_LOADS + B_LOADS;
   typedef typename Mfma<T>::frag frag;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][STAGE_BYTES];
 
   const int K = p.K;
   const int KT = K / BK;
-  const int tiles_m = (int)((p.M + BM - 1) / BM);
+  const int tiles_m = (int)((p.M - m_begin + BM - 1) / BM);
   const int tiles_n = p.N / BN;
   const int total = tiles_m * tiles_n;
   // XCD-aware tile order (see the file comment)
@@ -148,7 +159,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
   const int in_group = t - group * GROUP_M * tiles_n;
   const int tm = first_m + in_group % gsize;
   const int tn = in_group / gsize;
-  const int64_t m0 = (int64_t)tm * BM;
+  const int64_t m0 = m_begin + (int64_t)tm * BM;
   const int n0 = tn * BN;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -161,12 +172,13 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bw + (int64_t)n0 * K, (int64_t)BN * K * 2);
 
   // Direct-to-LDS load plan: a 1 KiB wave instruction fills 16 rows; wave w
-  // fills rows 64w .. 64w+63 of each operand (4 instructions each).  Lane l
-  // writes row 16c + l/4 at physical slot l%4, so it fetches logical slot
-  // (l%4) ^ ((l >> 4) & 3).  The whole offset is in the VGPR operand, which
-  // is what the buffer range check covers (rows past M read as zero).
-  const uint32_t voff = (uint32_t)(((wave * ROWS_PER_WAVE_LOAD + (lane >> 2)) * K +
-                                    (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
+  // fills rows (BM/8) w .. of A and 32 w .. 32 w + 31 of B.  Lane l writes
+  // row 16c + l/4 of its chunk at physical slot l%4, so it fetches logical
+  // slot (l%4) ^ ((l >> 4) & 3).  The whole offset is in the VGPR operand,
+  // which is what the buffer range check covers (rows past M read as zero).
+  const uint32_t lane_off = (uint32_t)(((lane >> 2) * K + (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
+  const uint32_t a_off = lane_off + (uint32_t)(wave * A_LOADS * 16 * K * 2);
+  const uint32_t b_off = lane_off + (uint32_t)(wave * B_LOADS * 16 * K * 2);
   const uint32_t chunk_stride = (uint32_t)(16 * K * 2);
 
   // A step past the last one is issued at an offset beyond the descriptor's
@@ -177,18 +189,22 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
     const bool valid = kt < KT;
     const uint32_t kbyte = (uint32_t)(kt * BK * 2);
 #pragma unroll
-    for (int c = 0; c < ROWS_PER_WAVE_LOAD / 16; ++c) {
-      const uint32_t off = valid ? voff + c * chunk_stride + kbyte : 0x80000000u;
-      const int chunk = wave * (ROWS_PER_WAVE_LOAD / 16) + c;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + chunk * 1024), 16, off, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(st + OP_BYTES + chunk * 1024), 16,
+    for (int c = 0; c < A_LOADS; ++c) {
+      const uint32_t off = valid ? a_off + c * chunk_stride + kbyte : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * A_LOADS + c) * 1024), 16,
                                                off, 0, 0, 0);
+    }
+#pragma unroll
+    for (int c = 0; c < B_LOADS; ++c) {
+      const uint32_t off = valid ? b_off + c * chunk_stride + kbyte : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (lds_ptr_t)(st + A_BYTES + (wave * B_LOADS + c) * 1024), 16, off, 0, 0, 0);
     }
   };
 
-  f32x16 acc[4][NJ];
+  f32x16 acc[MI][NJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
@@ -196,29 +212,30 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
 
   // fragment addressing: lane reads row (block + lane%32), k-slot kk*2 + lane/32
   const int r32 = lane & 31, hi = lane >> 5, sw = (lane >> 2) & 3;
-  const int a_row0 = (wm * 128 + r32) * 64;  // byte offset of this lane's first A row
+  const int a_row0 = (wm * (BM / 2) + r32) * 64;  // byte offset of this lane's first A row
   const int b_row0 = (wn * WN + r32) * 64;
 
-  frag fx[2][4], fw[2][NJ];
-  auto read_frags = [&](const uint8_t* st, int kk, frag (&x)[4], frag (&wv)[NJ]) {
+  frag fx[2][MI], fw[2][NJ];
+  auto read_frags = [&](const uint8_t* st, int kk, frag (&x)[MI], frag (&wv)[NJ]) {
     const int so = (((kk * 2 + hi) ^ sw) * 16);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
       x[i] = *reinterpret_cast<const frag*>(st + a_row0 + i * 32 * 64 + so);
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
-      wv[j] = *reinterpret_cast<const frag*>(st + OP_BYTES + b_row0 + j * 32 * 64 + so);
+      wv[j] = *reinterpret_cast<const frag*>(st + A_BYTES + b_row0 + j * 32 * 64 + so);
   };
-  auto mfma16 = [&](const frag (&x)[4], const frag (&wv)[NJ]) {
+  auto mfma_step = [&](const frag (&x)[MI], const frag (&wv)[NJ]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < NJ; ++j) acc[i][j] = Mfma<T>::run(wv[j], x[i], acc[i][j]);
   };
+  constexpr int NR = MI + NJ, NM = MI * NJ;  // LDS reads and MFMAs per k-step
 
   // prologue: steps 0 .. NS-2 in flight; step 0 must land
   for (int s = 0; s < NS - 1; ++s) issue(s);
-  stage_barrier(NS - 2);
+  stage_barrier<LPS>(NS - 2);
   read_frags(smem[0], 0, fx[0], fw[0]);
   for (int kt = 0; kt < KT; ++kt) {
     // The stage refilled here was consumed at step kt-1, and every wave has
@@ -228,30 +245,30 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
     const uint8_t* st = smem[kt % NS];
     issue(kt + NS - 1);
     read_frags(st, 1, fx[1], fw[1]);
-    mfma16(fx[0], fw[0]);
+    mfma_step(fx[0], fw[0]);
 #pragma unroll
-    for (int g = 0; g < 4 + NJ; ++g) {
-      if (g < LOADS_PER_STAGE) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                          // LDS read
-      if (g < 4 * NJ) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // MFMA
+    for (int g = 0; g < NR; ++g) {
+      if (g < LPS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                // LDS read
+      if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4 * NJ - (4 + NJ), 0);
+    if (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
     // step kt+1 must have landed; the loads of steps kt+2, kt+3 stay in flight
-    stage_barrier(NS - 2);
+    stage_barrier<LPS>(NS - 2);
     // k-step 1, with the first fragments of step kt+1 read meanwhile (after
     // the last step this reads a stage nobody uses)
     read_frags(smem[(kt + 1) % NS], 0, fx[0], fw[0]);
-    mfma16(fx[1], fw[1]);
+    mfma_step(fx[1], fw[1]);
 #pragma unroll
-    for (int g = 0; g < 4 + NJ; ++g) {
+    for (int g = 0; g < NR; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4 * NJ - (4 + NJ), 0);
+    if (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
   }
 
-  // Epilogue.  acc[i][j][r] = C[m][n] with m = m0 + wm*128 + i*32 + r32 and
-  // n = n0 + wn*128 + j*32 + 8*(r/4) + 4*hi + r%4.  Every input of a row group
+  // Epilogue.  acc[i][j][r] = C[m][n] with m = m0 + wm*(BM/2) + i*32 + r32 and
+  // n = n0 + wn*64 + j*32 + 8*(r/4) + 4*hi + r%4.  Every input of a row group
   // is loaded before any of its stores (the pointers are restrict), so the
   // loads overlap instead of each paying a full memory latency.
   float bv[NJ][4][4];
@@ -262,8 +279,8 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
       load4f<uint16_t>(bias + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, bv[j][q]);
   const int64_t rpb = p.c_map.rows_per_batch;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t m = m0 + wm * 128 + i * 32 + r32;
+  for (int i = 0; i < MI; ++i) {
+    const int64_t m = m0 + wm * (BM / 2) + i * 32 + r32;
     if (m >= p.M) continue;
     const int64_t b = m / rpb;
     const int64_t within = m - b * rpb;
@@ -313,42 +330,73 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, const uin
   }
 }
 
+// Rows [0, split) go in 256-row tiles, rows [split, M) in 128-row tiles.  The
+// split minimises an estimate of the time in units of one wave of 256-row
+// tiles over the 256 CUs: a wave of 128-row tiles costs 0.62 (measured: the
+// half-height tile does half the MFMA work at lower efficiency), and a
+// second launch behind the first costs about 3072/K waves (its start-up and
+// the first launch's drain, measured at roughly 50 us).  E.g. 17776 x 3072 x
+// 12288: 840 tiles = 4 waves, or 768 + 132 half tiles = 3 + 0.62 + 0.25.
+static int64_t gemm_row_split(int64_t M, int tiles_n, int K) {
+  constexpr int CUS = 256;
+  auto waves = [&](int64_t tiles) { return (double)((tiles + CUS - 1) / CUS); };
+  const int64_t tm = (M + 255) / 256;
+  int64_t best_split = M;
+  double best = waves(tm * tiles_n);
+  for (int64_t t1 = tm - 1; t1 >= 0 && t1 >= tm - 16; --t1) {
+    const int64_t rest = (M - t1 * 256 + 127) / 128;
+    const double cost = waves(t1 * tiles_n) + 0.62 * waves(rest * tiles_n) + (t1 > 0 ? 3072.0 / K : 0.0);
+    if (cost < best - 1e-9) { best = cost; best_split = t1 * 256; }
+  }
+  return best_split;
+}
+
+template <typename T, int EPI, typename CT, typename RT>
+static hipError_t launch_t(const GemmParams& p, hipStream_t s) {
+  const int tiles_n = p.N / BN;
+  const int64_t split = gemm_row_split(p.M, tiles_n, p.K);
+  if (split > 0) {
+    const int64_t tiles = ((split + 255) / 256) * tiles_n;
+    GemmParams q = p;
+    q.M = split;
+    hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT, 256>), dim3((unsigned)tiles), dim3(NWAVES * 64), 0, s,
+                       q, (int64_t)0, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
+  }
+  if (split < p.M) {
+    const int64_t tiles = ((p.M - split + 127) / 128) * tiles_n;
+    hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT, 128>), dim3((unsigned)tiles), dim3(NWAVES * 64), 0, s,
+                       p, split, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
-  const int64_t tiles = ((p.M + BM - 1) / BM) * (p.N / BN);
-  if (tiles == 0) return hipSuccess;
-  const dim3 grid((unsigned)tiles), block(NWAVES * 64);
-#define XEMA_GEMM(T, EPI, CT, RT)                                                          \
-  hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT>), grid, block, 0, s, p, p.bias, (CT*)p.c,    \
-                     (const RT*)p.resid, p.gate)
+  if (p.M <= 0) return hipSuccess;
   const bool h = p.dtype == XEMA_F16;
   switch (p.epilogue) {
     case XEMA_EPI_BIAS:
     case XEMA_EPI_BIAS_GELU: {
       const bool gelu = p.epilogue == XEMA_EPI_BIAS_GELU;
       const bool ch = p.c_dtype == XEMA_F16;
-      if (h && ch && gelu) XEMA_GEMM(f16, XEMA_EPI_BIAS_GELU, f16, float);
-      else if (h && ch) XEMA_GEMM(f16, XEMA_EPI_BIAS, f16, float);
-      else if (h && gelu) XEMA_GEMM(f16, XEMA_EPI_BIAS_GELU, bf16, float);
-      else if (h) XEMA_GEMM(f16, XEMA_EPI_BIAS, bf16, float);
-      else if (ch && gelu) XEMA_GEMM(bf16, XEMA_EPI_BIAS_GELU, f16, float);
-      else if (ch) XEMA_GEMM(bf16, XEMA_EPI_BIAS, f16, float);
-      else if (gelu) XEMA_GEMM(bf16, XEMA_EPI_BIAS_GELU, bf16, float);
-      else XEMA_GEMM(bf16, XEMA_EPI_BIAS, bf16, float);
-      break;
+      if (h && ch && gelu) return launch_t<f16, XEMA_EPI_BIAS_GELU, f16, float>(p, s);
+      if (h && ch) return launch_t<f16, XEMA_EPI_BIAS, f16, float>(p, s);
+      if (h && gelu) return launch_t<f16, XEMA_EPI_BIAS_GELU, bf16, float>(p, s);
+      if (h) return launch_t<f16, XEMA_EPI_BIAS, bf16, float>(p, s);
+      if (ch && gelu) return launch_t<bf16, XEMA_EPI_BIAS_GELU, f16, float>(p, s);
+      if (ch) return launch_t<bf16, XEMA_EPI_BIAS, f16, float>(p, s);
+      if (gelu) return launch_t<bf16, XEMA_EPI_BIAS_GELU, bf16, float>(p, s);
+      return launch_t<bf16, XEMA_EPI_BIAS, bf16, float>(p, s);
     }
     case XEMA_EPI_GATED_RESIDUAL: {
       const bool rf = p.resid_dtype == XEMA_F32;
-      if (h && rf) XEMA_GEMM(f16, XEMA_EPI_GATED_RESIDUAL, float, float);
-      else if (h) XEMA_GEMM(f16, XEMA_EPI_GATED_RESIDUAL, float, uint16_t);
-      else if (rf) XEMA_GEMM(bf16, XEMA_EPI_GATED_RESIDUAL, float, float);
-      else XEMA_GEMM(bf16, XEMA_EPI_GATED_RESIDUAL, float, uint16_t);
-      break;
+      if (h && rf) return launch_t<f16, XEMA_EPI_GATED_RESIDUAL, float, float>(p, s);
+      if (h) return launch_t<f16, XEMA_EPI_GATED_RESIDUAL, float, uint16_t>(p, s);
+      if (rf) return launch_t<bf16, XEMA_EPI_GATED_RESIDUAL, float, float>(p, s);
+      return launch_t<bf16, XEMA_EPI_GATED_RESIDUAL, float, uint16_t>(p, s);
     }
     default:
       return hipErrorInvalidValue;
   }
-#undef XEMA_GEMM
-  return hipGetLastError();
 }
 
 }  // namespace xema

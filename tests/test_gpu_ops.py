@@ -163,6 +163,46 @@ def test_gemm_rows_independent_of_m():
     assert torch.equal(outs[0][300:377], outs[2])
 
 
+@pytest.mark.parametrize("M,N,K,epi", [
+    (16584, 3072, 12288, X.XEMA_EPI_GATED_RESIDUAL),   # 256-row tiles + a 128-row tail launch
+    (17776, 12288, 3072, X.XEMA_EPI_BIAS_GELU),        # 256-row tiles only
+])
+def test_gemm_tile_heights_agree_at_full_size(M, N, K, epi):
+    """Large calls run 256-row tiles (and, where that fills the CUs better, a
+    second launch of 128-row tiles over the last rows); small calls run
+    128-row tiles.  Rows around the split and elsewhere are bit-identical to
+    the same rows computed by a small call, and sampled rows match fp64."""
+    g = torch.Generator(device=DEV).manual_seed(M + N)
+    a = torch.randn(M, K, device=DEV, generator=g).half()
+    b = (torch.randn(N, K, device=DEV, generator=g) / np.sqrt(K)).half()
+    bias = (torch.randn(N, device=DEV, generator=g) * 0.02).to(torch.bfloat16)
+    gated = epi == X.XEMA_EPI_GATED_RESIDUAL
+    cdt, c_dtype = (torch.float32, X.XEMA_F32) if gated else (torch.float16, X.XEMA_F16)
+    res = torch.randn(M, N, device=DEV, generator=g) if gated else None
+    gate = torch.randn(N, device=DEV, generator=g) if gated else None
+
+    def run(r0, rows):
+        C = torch.empty((rows, N), dtype=cdt, device=DEV)
+        kw = dict(resid=res[r0:], resid_dtype=X.XEMA_F32, ld_resid=N, gate=gate, gate_stride=0) if gated else {}
+        X.xema_op_gemm(X.gemm_args(X.XEMA_F16, a[r0:], rows, K, b, N, bias, epi, C, c_dtype, N, **kw))
+        return C
+
+    full = run(0, M)
+    for r0, rows in ((16300, 200), (0, 96), (M - 150, 150)):
+        part = run(r0, rows)
+        torch.cuda.synchronize()
+        assert torch.equal(full[r0:r0 + rows], part), (r0, rows)
+    pick = np.array([0, 1, 16383, 16384, 16385, M // 2, M - 1])
+    a64 = a[pick].double().cpu().numpy()
+    acc = a64 @ b.double().cpu().numpy().T + bias.double().cpu().numpy()
+    if gated:
+        ref = res[pick].double().cpu().numpy() + gate.double().cpu().numpy() * acc
+        rel = 1e-6
+    else:
+        ref, rel = O.gelu_tanh(acc), 2.0 ** -10
+    _check_close(full[pick].float().cpu().numpy(), ref, rel, 2e-5 * np.sqrt(K), f"gemm {M}x{N}x{K}")
+
+
 def test_convert_f16_matches_torch():
     g = _rng(12)
     vals = np.concatenate([g.standard_normal(4096) * s for s in (1e-7, 1e-4, 1.0, 1e3)])
