@@ -148,11 +148,10 @@ struct WaveState {
 };
 
 // S^T = K Q^T - mrow for two 32-key blocks x QB query columns
-template <int HD, int QB>
+template <int HD, int QB, bool MI>
 __device__ __forceinline__ void tile_scores(const uint8_t* Ks, const f16x8 (&qf)[QB][HD / 16],
                                             const f32x16 (&minit)[QB], int krow, int kswz, int hi,
                                             f32x16 (&s)[2][QB]) {
-  constexpr bool MI = minit_in_mfma(QB);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int row = kb * 32 + krow;
@@ -310,13 +309,13 @@ __device__ __forceinline__ void att_iter(uint8_t (*smem)[2 * KV * HD * 2], int k
                                             (uint32_t)((kv + 1) * KV * 2));
   const uint8_t* cur = smem[kv % 3];
   if (lead) {
-    tile_scores<HD, QB>(cur, qf, st.minit, krow, kswz, hi, s);
+    tile_scores<HD, QB, minit_in_mfma(QB)>(cur, qf, st.minit, krow, kswz, hi, s);
     if (LAST && tail < KV) mask_tail<QB>(s, tail, hi);
     tile_softmax<HD, QB>(s, kv == 0, st, pf);
     tile_pv<HD, QB>(cur + K_BYTES, pf, r32, hi, st.oacc);
   } else {
     if (kv > 0) tile_pv<HD, QB>(smem[(kv + 2) % 3] + K_BYTES, pf, r32, hi, st.oacc);
-    tile_scores<HD, QB>(cur, qf, st.minit, krow, kswz, hi, s);
+    tile_scores<HD, QB, minit_in_mfma(QB)>(cur, qf, st.minit, krow, kswz, hi, s);
     if (LAST && tail < KV) mask_tail<QB>(s, tail, hi);
     tile_softmax<HD, QB>(s, kv == 0, st, pf);
   }
@@ -464,7 +463,7 @@ __device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int 
                                             (uint32_t)((kv + 1) * KV * 2));
   f32x16 s[2][QB];
   f16x8 pf[QB][2][2];
-  tile_scores<HD, QB>(smem[stage], qf, st.minit, krow, kswz, hi, s);
+  tile_scores<HD, QB, false>(smem[stage], qf, st.minit, krow, kswz, hi, s);
   if (LAST && tail < KV) mask_tail<QB>(s, tail, hi);
   tile_softmax_maxtrig<HD, QB>(s, kv == 0, st, pf);
   tile_pv<HD, QB>(smem[stage] + K_BYTES, pf, r32, hi, st.oacc);
