@@ -1,9 +1,11 @@
 """Benchmark: one DiT block forward step on one MI355X.
 
-Workload: the 480x720x49f video request (13 x 30 x 45 latent grid + 226 text
-tokens = 17776 tokens), hidden 3072, 48 heads x 64, MLP 12288, batch 1, under
-a 2 GiB activation budget (the plan runs it unchunked).  Synthetic seeded
-inputs and random weights, resident in HBM before timing starts.
+Default workload: the 480x720x49f video request (13 x 30 x 45 latent grid +
+226 text tokens = 17776 tokens), hidden 3072, 48 heads x 64, MLP 12288,
+batch 1, under a 2 GiB activation budget (the plan runs it unchunked).
+--workload picks another of the five block configurations, --budget or
+--chunk another chunking.  Synthetic seeded inputs and random weights,
+resident in HBM before timing starts.
 
 Prints one JSON line: whole-step throughput (TFLOP/s of the block's
 algorithmic FLOPs), ms per step, the roofline of the dominant kernel
@@ -30,6 +32,11 @@ def attention_flops(B, H, L, d, q_count=None):
     return 4 * B * H * q_count * L * d
 
 
+# default activation budget per workload (arena bytes)
+DEFAULT_BUDGET = {"tiny": 1 << 30, "image": 2 << 30, "image_b4": 2 << 30, "video": 2 << 30,
+                  "highres": 32 * 10**9, "long": 8 << 30}
+
+
 def bench_gpu(args, shape):
     import numpy as np
     import torch
@@ -50,7 +57,10 @@ def bench_gpu(args, shape):
     cfg = X.block_cfg(shape.hidden, shape.heads, shape.head_dim, shape.mlp_hidden, shape.cond_dim,
                       shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps)
     req = X.request(shape.batch, shape.text_len, *shape.grid)
-    plan = X.xema_workspace_plan(cfg, req, args.budget)
+    if args.chunk is not None:
+        plan = X.xema_workspace_layout(cfg, req, args.chunk)
+    else:
+        plan = X.xema_workspace_plan(cfg, req, args.budget)
     ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=dev)
     out = torch.empty((shape.batch, shape.seq_len, shape.hidden), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -174,12 +184,30 @@ def cpu_baseline(shape, n_rows):
     }
 
 
+WORKLOAD_TEXT = {
+    "tiny": "tiny DiT block: 32 text + 1x16x16 visual tokens (L=288), D=256, 4x64 heads, MLP 1024, batch 1",
+    "image": "image DiT block 1024x1024: 512 text + 1x64x64 visual tokens (L=4608), D=3072, 24x128 heads, "
+             "MLP 12288, batch 1",
+    "image_b4": "image DiT block 1024x1024: 512 text + 1x64x64 visual tokens (L=4608), D=3072, 24x128 heads, "
+                "MLP 12288, batch 4",
+    "video": "video DiT block 480x720x49f: 226 text + 13x30x45 visual tokens (L=17776), D=3072, 48x64 heads, "
+             "MLP 12288, batch 1",
+    "highres": "high-res video DiT block 1080p x49f: 226 text + 13x68x120 visual tokens (L=106306), D=3072, "
+               "48x64 heads, MLP 12288, batch 1",
+    "long": "long video DiT block: 1024 text + 33x22x38 visual tokens (L=28612), D=4096, 32x128 heads, "
+            "MLP 16384, batch 2",
+}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--budget", type=int, default=2 << 30, help="activation budget (arena bytes)")
+    ap.add_argument("--workload", default="video", help="tiny, image, image_b4, video, highres or long")
+    ap.add_argument("--budget", type=int, default=None,
+                    help="activation budget (arena bytes); default per workload, 2 GiB for video")
+    ap.add_argument("--chunk", type=int, default=None, help="chunk_tokens instead of the planned one")
     ap.add_argument("--cpu-rows", type=int, default=3072)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -196,7 +224,9 @@ def main():
         sys.exit(2)
 
     import workloads as W
-    shape = W.VIDEO
+    shape = W.CONFIGS[args.workload]
+    if args.budget is None:
+        args.budget = DEFAULT_BUDGET[args.workload]
     g = bench_gpu(args, shape)
     flops = shape.flops()
     tflops = flops / (g["ms"] * 1e-3) / 1e12
@@ -219,15 +249,15 @@ def main():
         "data": "synthetic (seeded N(0,1) tokens and conditioning, N(0,1/fan_in) random weights)",
         "frac_peak": round(tflops / PEAK_TFLOPS, 4),
         "config": {
-            "workload": "video DiT block 480x720x49f: 226 text + 13x30x45 visual tokens (L=17776), "
-                        "D=3072, 48x64 heads, MLP 12288, batch 1",
+            "workload": WORKLOAD_TEXT[args.workload],
             "batch": B, "seq_len": L, "hidden": shape.hidden, "heads": H, "head_dim": d,
             "mlp_hidden": shape.mlp_hidden, "flops_per_step": flops,
             "budget_bytes": args.budget, "chunk_tokens": plan.chunk_tokens,
             "arena_bytes": plan.workspace_bytes, "device_peak_bytes": g["device_peak_bytes"],
         },
         "roofline": {
-            "kernel": "k_attention_lazy<64> (joint attention, all 17776 queries x 17776 keys x 48 heads)",
+            "kernel": (f"{'k_attention_lazy<64>' if d == 64 else 'k_attention<128>'} (joint attention, "
+                       f"all {L} queries x {L} keys x {B * H} batch-heads)"),
             "bound": "mfma",
             "achieved": round(attn_tflops, 2),
             "peak": PEAK_TFLOPS,
@@ -235,10 +265,10 @@ def main():
             "frac": round(attn_tflops / PEAK_TFLOPS, 4),
             "ms_per_launch": round(g["attn_ms"], 4),
             "flops_per_launch": af,
-            "traffic": measured_traffic(),
+            "traffic": measured_traffic() if args.workload == "video" else None,
         },
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == "video":
         result["cpu_baseline"] = cpu_baseline(shape, args.cpu_rows)
     print(json.dumps(result), flush=True)
 
