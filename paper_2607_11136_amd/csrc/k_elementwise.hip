@@ -186,7 +186,8 @@ __global__ __launch_bounds__(256) void k_qk_norm_rope(QkRopeArgs a) {
 
   if (tid < TOK) {
     const int vi = a.tok_begin + t0 + tid - a.text_len;
-    const int gw = a.geom.grid[2], hw = a.geom.grid[1] * gw;
+    // (a text-only request has an empty grid; its tokens never reach the division)
+    const int gw = max(a.geom.grid[2], 1), hw = max(a.geom.grid[1] * a.geom.grid[2], 1);
     tpos[tid][0] = vi < 0 ? -1 : vi / hw;
     tpos[tid][1] = vi < 0 ? 0 : (vi % hw) / gw;
     tpos[tid][2] = vi < 0 ? 0 : vi % gw;

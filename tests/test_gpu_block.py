@@ -120,6 +120,32 @@ def test_batch_rows_are_independent_runs():
         assert torch.equal(o1[0], full[b]), b
 
 
+# Degenerate request shapes: text only (empty grid), visual only (no text),
+# a sequence shorter than one 64-key tile, with extreme chunkings.
+EDGE = {
+    "text_only": W.tiny_shape(name="text_only", cfg_id=60, batch=2, text_len=100, grid=(0, 0, 0),
+                              hidden=256, heads=4, head_dim=64, mlp_hidden=512, cond_dim=256,
+                              rope_dims=(16, 24, 24)),
+    "visual_only": W.tiny_shape(name="visual_only", cfg_id=61, batch=1, text_len=0, grid=(2, 5, 7),
+                                hidden=256, heads=2, head_dim=128, mlp_hidden=256, cond_dim=256,
+                                rope_dims=(32, 48, 48)),
+    "short": W.tiny_shape(name="short", cfg_id=62, batch=2, text_len=5, grid=(1, 4, 8), hidden=512,
+                          heads=8, head_dim=64, mlp_hidden=1024, cond_dim=512, rope_dims=(16, 24, 24)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_shapes_match_oracle_and_chunk_exactly(name):
+    s = EDGE[name]
+    print(f"edge {name}: B={s.batch} L={s.seq_len} text={s.text_len} grid={s.grid}", flush=True)
+    dev = Device(W.make_inputs(s))
+    base, _, _ = dev.run(0)
+    assert_parity(base.cpu().numpy(), O.block_forward_shape(dev.inputs), f"edge {name}")
+    for chunk in (1, 7, s.seq_len - 1):
+        out, _, _ = dev.run(chunk)
+        assert torch.equal(out, base), (name, chunk)
+
+
 def test_budget_plan_drives_the_call():
     """Plan a budget between the smallest and the unchunked arena, run with the
     planned chunk in an arena of exactly the planned size."""
