@@ -9,6 +9,8 @@ Modules
   brute   the same definition as scalar pure-Python loops, for tiny shapes
   layout  Algorithm 1 (Sec. 6.1) and the "only as much as needed" chunk plan
           (Sec. 5.1, the pi* objective) over the block's slot table
+  offload the selective weight-offloading plan of an N-block step (Sec. 5.1)
+  step    an N-block step: the blocks applied in sequence (Sec. 2.1)
 
 Readings.  The paper names the DiT block but prints none of its arithmetic, so
 the following conventions are readings (they bind the oracle and the HIP path

@@ -11,7 +11,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Dict, Optional, Sequence
+from typing import Dict, List, Optional, Sequence
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libxema.so")
@@ -94,6 +94,19 @@ class GemmArgs(ctypes.Structure):
                 ("gate", ctypes.c_void_p), ("gate_stride", ctypes.c_int64)]
 
 
+XEMA_MAX_BLOCKS = 256
+
+
+class OffloadPlan(ctypes.Structure):
+    _fields_ = [("n_blocks", ctypes.c_int32), ("n_offloaded", ctypes.c_int32),
+                ("n_staging", ctypes.c_int32), ("offloaded", ctypes.c_int32 * XEMA_MAX_BLOCKS),
+                ("block_weight_bytes", ctypes.c_int64), ("resident_weight_bytes", ctypes.c_int64),
+                ("staging_bytes", ctypes.c_int64), ("device_weight_bytes", ctypes.c_int64)]
+
+    def offloaded_blocks(self) -> List[int]:
+        return [i for i in range(self.n_blocks) if self.offloaded[i]]
+
+
 _P = ctypes.c_void_p
 _I32, _I64, _F32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
 _SIGNATURES = {
@@ -117,6 +130,16 @@ _SIGNATURES = {
                                             _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "xema_op_attention": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _P, _P]),
     "xema_op_convert_f16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "xema_offload_plan_k": (ctypes.c_int, [ctypes.POINTER(BlockCfg), _I32, _I32, _I32,
+                                           ctypes.POINTER(OffloadPlan)]),
+    "xema_offload_plan_budget": (ctypes.c_int, [ctypes.POINTER(BlockCfg), _I32, _I64, _I32,
+                                                ctypes.POINTER(OffloadPlan)]),
+    "xema_step_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request),
+                                                 _I32, ctypes.POINTER(OffloadPlan),
+                                                 ctypes.POINTER(_I64)]),
+    "xema_dit_step_fwd": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
+                                         ctypes.POINTER(BlockWeights), ctypes.POINTER(OffloadPlan),
+                                         _P, _I32, _P, _I64, _P, _P, _P]),
 }
 EXPORTED = tuple(_SIGNATURES)
 
@@ -302,3 +325,47 @@ def xema_op_convert_f16(src, dst, n: int, stream=None) -> None:
 
 def padded_len(seq_len: int) -> int:
     return (seq_len + XEMA_SEQ_PAD - 1) // XEMA_SEQ_PAD * XEMA_SEQ_PAD
+
+
+# -- the N-block step with selective weight offloading (xema_step.h) ---------------
+
+
+def xema_offload_plan_k(cfg: BlockCfg, n_blocks: int, n_offloaded: int, n_staging: int = 2) -> OffloadPlan:
+    p = OffloadPlan()
+    _check(lib().xema_offload_plan_k(ctypes.byref(cfg), n_blocks, n_offloaded, n_staging,
+                                     ctypes.byref(p)), "xema_offload_plan_k")
+    return p
+
+
+def xema_offload_plan_budget(cfg: BlockCfg, n_blocks: int, weight_budget_bytes: int,
+                             n_staging: int = 2) -> OffloadPlan:
+    """Smallest K that fits the weight budget.  Raises XemaError
+    (XEMA_ERR_BUDGET_TOO_SMALL, with the K = n_blocks plan as `.plan`)."""
+    p = OffloadPlan()
+    st = lib().xema_offload_plan_budget(ctypes.byref(cfg), n_blocks, int(weight_budget_bytes),
+                                        n_staging, ctypes.byref(p))
+    if st != XEMA_OK:
+        e = XemaError(st, "xema_offload_plan_budget")
+        e.plan = p
+        raise e
+    return p
+
+
+def xema_step_workspace_bytes(cfg: BlockCfg, req: Request, chunk_tokens: int, plan: OffloadPlan) -> int:
+    n = _I64()
+    _check(lib().xema_step_workspace_bytes(ctypes.byref(cfg), ctypes.byref(req), chunk_tokens,
+                                           ctypes.byref(plan), ctypes.byref(n)),
+           "xema_step_workspace_bytes")
+    return n.value
+
+
+def xema_dit_step_fwd(cfg: BlockCfg, req: Request, tokens, weights: Sequence[BlockWeights],
+                      plan: OffloadPlan, cond, chunk_tokens: int, workspace, workspace_bytes: int,
+                      out, stream=None, copy_stream=None) -> None:
+    arr = (BlockWeights * len(weights))(*weights)
+    cs = None if copy_stream is None else (copy_stream if isinstance(copy_stream, int)
+                                           else copy_stream.cuda_stream)
+    _check(lib().xema_dit_step_fwd(ctypes.byref(cfg), ctypes.byref(req), _ptr(tokens), arr,
+                                   ctypes.byref(plan), _ptr(cond), chunk_tokens, _ptr(workspace),
+                                   int(workspace_bytes), _ptr(out), _stream(stream), cs),
+           "xema_dit_step_fwd")

@@ -209,6 +209,105 @@ extern "C" int xema_op_convert_f16(const void* src, void* dst, int64_t n, void* 
 // the block forward
 // ---------------------------------------------------------------------------
 
+namespace xema {
+
+// The block's launches on stream s, arguments already validated: x is
+// [B, L, D] bf16 or fp32 (x_dtype), the arena at ws follows `plan` for chunk
+// ch, out is [B, L, D] fp32.
+int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens, int x_dtype,
+              const xema_block_weights& w, const void* cond, int64_t ch, uint8_t* ws,
+              const xema_plan& plan, float* out, hipStream_t s) {
+  const int64_t B = r.batch, L = seq_len(r), D = c.hidden, F = c.mlp_hidden, Dc = c.cond_dim;
+  const int64_t Lp = padded_len(L);
+  auto slot = [&](int id) { return (void*)(ws + plan.slot_offset[id]); };
+  float* mod = (float*)slot(XEMA_SLOT_MOD);
+  float* rope = (float*)slot(XEMA_SLOT_ROPE);
+  void* Q = slot(XEMA_SLOT_Q);
+  void* Kk = slot(XEMA_SLOT_K);
+  void* VT = slot(XEMA_SLOT_VT);
+  void* ln1 = slot(XEMA_SLOT_LN1);
+  void* qkv = slot(XEMA_SLOT_QKV);
+  void* wo16 = slot(XEMA_SLOT_WO16);
+  void* wup16 = slot(XEMA_SLOT_WUP16);
+  void* wdown16 = slot(XEMA_SLOT_WDOWN16);
+  void* attn = slot(XEMA_SLOT_ATTN);
+  float* x1 = (float*)slot(XEMA_SLOT_X1);
+  void* ln2 = slot(XEMA_SLOT_LN2);
+  void* hid = slot(XEMA_SLOT_HID);
+  const RopeGeom geom = geom_of(c, r);
+
+#define XEMA_TRY(expr)                          \
+  do {                                          \
+    if ((expr) != hipSuccess) return XEMA_ERR_HIP; \
+  } while (0)
+
+  // step 0
+  XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_w,
+                        (const uint16_t*)w.ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s));
+  XEMA_TRY(launch_rope_table(geom, c.rope_theta, rope, s));
+
+  // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk
+  for (int64_t t0 = 0; t0 < L; t0 += ch) {
+    const int64_t cc = std::min(ch, L - t0);
+    const RowMap xmap{cc, L, t0};
+    XEMA_TRY(launch_ln_modulate(tokens, x_dtype, xmap, B * cc, (int)D, mod, mod + D, 6 * D,
+                                c.ln_eps, ln1, XEMA_BF16, s));
+    GemmParams g{};
+    g.dtype = XEMA_BF16; g.a = ln1; g.b = w.qkv_w; g.M = B * cc; g.N = (int)(3 * D); g.K = (int)D;
+    g.bias = (const uint16_t*)w.qkv_b; g.epilogue = XEMA_EPI_BIAS;
+    g.c = qkv; g.c_dtype = XEMA_F16; g.c_map = RowMap{cc, cc, 0}; g.ldc = 3 * D;
+    XEMA_TRY(launch_gemm(g, s));
+    const QkRopeArgs qa = qk_args(c, r, qkv, (int)t0, (int)cc, w.q_gamma, w.k_gamma, rope, Q, Kk, VT);
+    XEMA_TRY(launch_qk_norm_rope(qa, c.head_dim, s));
+  }
+
+  // step 4: fp16 copies of the phase-B weights
+  XEMA_TRY(launch_convert_f16((const uint16_t*)w.o_w, (_Float16*)wo16, D * D, s));
+  XEMA_TRY(launch_convert_f16((const uint16_t*)w.up_w, (_Float16*)wup16, F * D, s));
+  XEMA_TRY(launch_convert_f16((const uint16_t*)w.down_w, (_Float16*)wdown16, D * F, s));
+
+  // phase B: attention -> out-proj -> LN2 -> MLP, per query chunk
+  for (int64_t t0 = 0; t0 < L; t0 += ch) {
+    const int64_t cc = std::min(ch, L - t0);
+    const RowMap ident{cc, cc, 0};
+    AttnParams ap;
+    ap.q = (const _Float16*)Q; ap.k = (const _Float16*)Kk; ap.vt = (const _Float16*)VT;
+    ap.o = (_Float16*)attn; ap.batch = (int)B; ap.heads = c.heads; ap.seq_len = (int)L;
+    ap.padded_len = (int)Lp; ap.q_begin = (int)t0; ap.q_count = (int)cc;
+    XEMA_TRY(launch_attention(ap, c.head_dim, s));
+
+    GemmParams g{};
+    g.dtype = XEMA_F16; g.a = attn; g.b = wo16; g.M = B * cc; g.N = (int)D; g.K = (int)D;
+    g.bias = (const uint16_t*)w.o_b; g.epilogue = XEMA_EPI_GATED_RESIDUAL;
+    g.c = x1; g.c_dtype = XEMA_F32; g.c_map = ident; g.ldc = D;
+    g.resid = tokens; g.resid_dtype = x_dtype; g.resid_map = RowMap{cc, L, t0}; g.ld_resid = D;
+    g.gate = mod + 2 * D; g.gate_stride = 6 * D;
+    XEMA_TRY(launch_gemm(g, s));
+
+    XEMA_TRY(launch_ln_modulate(x1, XEMA_F32, ident, B * cc, (int)D, mod + 3 * D, mod + 4 * D,
+                                6 * D, c.ln_eps, ln2, XEMA_F16, s));
+
+    GemmParams u{};
+    u.dtype = XEMA_F16; u.a = ln2; u.b = wup16; u.M = B * cc; u.N = (int)F; u.K = (int)D;
+    u.bias = (const uint16_t*)w.up_b; u.epilogue = XEMA_EPI_BIAS_GELU;
+    u.c = hid; u.c_dtype = XEMA_F16; u.c_map = ident; u.ldc = F;
+    XEMA_TRY(launch_gemm(u, s));
+
+    GemmParams d{};
+    d.dtype = XEMA_F16; d.a = hid; d.b = wdown16; d.M = B * cc; d.N = (int)D; d.K = (int)F;
+    d.bias = (const uint16_t*)w.down_b; d.epilogue = XEMA_EPI_GATED_RESIDUAL;
+    d.c = out; d.c_dtype = XEMA_F32; d.c_map = RowMap{cc, L, t0}; d.ldc = D;
+    d.resid = x1; d.resid_dtype = XEMA_F32; d.resid_map = ident; d.ld_resid = D;
+    d.gate = mod + 5 * D; d.gate_stride = 6 * D;
+    XEMA_TRY(launch_gemm(d, s));
+  }
+#undef XEMA_TRY
+  return XEMA_OK;
+}
+
+}  // namespace xema
+
+
 extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
                                   const void* tokens, const xema_block_weights* w,
                                   const void* cond, int32_t chunk_tokens, void* workspace,
@@ -228,12 +327,10 @@ extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request*
 
   const xema_block_cfg& c = *cfg;
   const xema_request& r = *req;
-  const int64_t B = r.batch, L = seq_len(r), D = c.hidden, F = c.mlp_hidden, Dc = c.cond_dim;
-  const int64_t Lp = padded_len(L);
+  const int64_t B = r.batch, L = seq_len(r), D = c.hidden, Dc = c.cond_dim;
   const int64_t out_bytes = B * L * D * 4;
-  const int64_t wbytes[12] = {6 * D * Dc * 2, 6 * D * 2, 3 * D * D * 2, 3 * D * 2,
-                              (int64_t)c.head_dim * 2, (int64_t)c.head_dim * 2, D * D * 2, D * 2,
-                              F * D * 2, F * 2, D * F * 2, D * 2};
+  int64_t wbytes[12];
+  block_weight_sizes(c, wbytes);
   // out is written while everything else is read: it must overlap nothing
   if (overlaps(out, out_bytes, tokens, B * L * D * 2) ||
       overlaps(out, out_bytes, cond, B * Dc * 2) ||
@@ -253,91 +350,7 @@ extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request*
   st = layout_for_chunk(c, r, ch, &plan);
   if (st != XEMA_OK) return st;
   if (workspace_bytes < plan.workspace_bytes) return XEMA_ERR_WORKSPACE_TOO_SMALL;
-
-  uint8_t* ws = (uint8_t*)workspace;
-  auto slot = [&](int id) { return (void*)(ws + plan.slot_offset[id]); };
-  float* mod = (float*)slot(XEMA_SLOT_MOD);
-  float* rope = (float*)slot(XEMA_SLOT_ROPE);
-  void* Q = slot(XEMA_SLOT_Q);
-  void* Kk = slot(XEMA_SLOT_K);
-  void* VT = slot(XEMA_SLOT_VT);
-  void* ln1 = slot(XEMA_SLOT_LN1);
-  void* qkv = slot(XEMA_SLOT_QKV);
-  void* wo16 = slot(XEMA_SLOT_WO16);
-  void* wup16 = slot(XEMA_SLOT_WUP16);
-  void* wdown16 = slot(XEMA_SLOT_WDOWN16);
-  void* attn = slot(XEMA_SLOT_ATTN);
-  float* x1 = (float*)slot(XEMA_SLOT_X1);
-  void* ln2 = slot(XEMA_SLOT_LN2);
-  void* hid = slot(XEMA_SLOT_HID);
-  const hipStream_t s = (hipStream_t)stream;
-  const RopeGeom geom = geom_of(c, r);
-
-#define XEMA_TRY(expr)                          \
-  do {                                          \
-    if ((expr) != hipSuccess) return XEMA_ERR_HIP; \
-  } while (0)
-
-  // step 0
-  XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w->ada_w,
-                        (const uint16_t*)w->ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s));
-  XEMA_TRY(launch_rope_table(geom, c.rope_theta, rope, s));
-
-  // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk
-  for (int64_t t0 = 0; t0 < L; t0 += ch) {
-    const int64_t cc = std::min(ch, L - t0);
-    const RowMap xmap{cc, L, t0};
-    XEMA_TRY(launch_ln_modulate(tokens, XEMA_BF16, xmap, B * cc, (int)D, mod, mod + D, 6 * D,
-                                c.ln_eps, ln1, XEMA_BF16, s));
-    GemmParams g{};
-    g.dtype = XEMA_BF16; g.a = ln1; g.b = w->qkv_w; g.M = B * cc; g.N = (int)(3 * D); g.K = (int)D;
-    g.bias = (const uint16_t*)w->qkv_b; g.epilogue = XEMA_EPI_BIAS;
-    g.c = qkv; g.c_dtype = XEMA_F16; g.c_map = RowMap{cc, cc, 0}; g.ldc = 3 * D;
-    XEMA_TRY(launch_gemm(g, s));
-    const QkRopeArgs qa = qk_args(c, r, qkv, (int)t0, (int)cc, w->q_gamma, w->k_gamma, rope, Q, Kk, VT);
-    XEMA_TRY(launch_qk_norm_rope(qa, c.head_dim, s));
-  }
-
-  // step 4: fp16 copies of the phase-B weights
-  XEMA_TRY(launch_convert_f16((const uint16_t*)w->o_w, (_Float16*)wo16, D * D, s));
-  XEMA_TRY(launch_convert_f16((const uint16_t*)w->up_w, (_Float16*)wup16, F * D, s));
-  XEMA_TRY(launch_convert_f16((const uint16_t*)w->down_w, (_Float16*)wdown16, D * F, s));
-
-  // phase B: attention -> out-proj -> LN2 -> MLP, per query chunk
-  for (int64_t t0 = 0; t0 < L; t0 += ch) {
-    const int64_t cc = std::min(ch, L - t0);
-    const RowMap ident{cc, cc, 0};
-    AttnParams ap;
-    ap.q = (const _Float16*)Q; ap.k = (const _Float16*)Kk; ap.vt = (const _Float16*)VT;
-    ap.o = (_Float16*)attn; ap.batch = (int)B; ap.heads = c.heads; ap.seq_len = (int)L;
-    ap.padded_len = (int)Lp; ap.q_begin = (int)t0; ap.q_count = (int)cc;
-    XEMA_TRY(launch_attention(ap, c.head_dim, s));
-
-    GemmParams g{};
-    g.dtype = XEMA_F16; g.a = attn; g.b = wo16; g.M = B * cc; g.N = (int)D; g.K = (int)D;
-    g.bias = (const uint16_t*)w->o_b; g.epilogue = XEMA_EPI_GATED_RESIDUAL;
-    g.c = x1; g.c_dtype = XEMA_F32; g.c_map = ident; g.ldc = D;
-    g.resid = tokens; g.resid_dtype = XEMA_BF16; g.resid_map = RowMap{cc, L, t0}; g.ld_resid = D;
-    g.gate = mod + 2 * D; g.gate_stride = 6 * D;
-    XEMA_TRY(launch_gemm(g, s));
-
-    XEMA_TRY(launch_ln_modulate(x1, XEMA_F32, ident, B * cc, (int)D, mod + 3 * D, mod + 4 * D,
-                                6 * D, c.ln_eps, ln2, XEMA_F16, s));
-
-    GemmParams u{};
-    u.dtype = XEMA_F16; u.a = ln2; u.b = wup16; u.M = B * cc; u.N = (int)F; u.K = (int)D;
-    u.bias = (const uint16_t*)w->up_b; u.epilogue = XEMA_EPI_BIAS_GELU;
-    u.c = hid; u.c_dtype = XEMA_F16; u.c_map = ident; u.ldc = F;
-    XEMA_TRY(launch_gemm(u, s));
-
-    GemmParams d{};
-    d.dtype = XEMA_F16; d.a = hid; d.b = wdown16; d.M = B * cc; d.N = (int)D; d.K = (int)F;
-    d.bias = (const uint16_t*)w->down_b; d.epilogue = XEMA_EPI_GATED_RESIDUAL;
-    d.c = out; d.c_dtype = XEMA_F32; d.c_map = RowMap{cc, L, t0}; d.ldc = D;
-    d.resid = x1; d.resid_dtype = XEMA_F32; d.resid_map = ident; d.ld_resid = D;
-    d.gate = mod + 5 * D; d.gate_stride = 6 * D;
-    XEMA_TRY(launch_gemm(d, s));
-  }
-#undef XEMA_TRY
-  return XEMA_OK;
+  return run_block(c, r, tokens, XEMA_BF16, *w, cond, ch, (uint8_t*)workspace, plan, (float*)out,
+                   (hipStream_t)stream);
 }
+

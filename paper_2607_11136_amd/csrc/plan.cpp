@@ -100,6 +100,13 @@ int validate_shapes(const xema_block_cfg* cfg, const xema_request* req) {
   return XEMA_OK;
 }
 
+void block_weight_sizes(const xema_block_cfg& c, int64_t bytes[12]) {
+  const int64_t D = c.hidden, F = c.mlp_hidden, Dc = c.cond_dim, d = c.head_dim;
+  const int64_t b[12] = {6 * D * Dc * 2, 6 * D * 2, 3 * D * D * 2, 3 * D * 2, d * 2, d * 2,
+                         D * D * 2,      D * 2,     F * D * 2,     F * 2,     D * F * 2, D * 2};
+  for (int i = 0; i < 12; ++i) bytes[i] = b[i];
+}
+
 int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
                      xema_plan* out) {
   const int64_t B = req.batch, D = cfg.hidden, F = cfg.mlp_hidden;

@@ -30,4 +30,23 @@ inline int64_t effective_chunk(int64_t L, int64_t chunk) {
 int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
                      xema_plan* out);
 
+// Bytes of one block's twelve weight tensors (order of xema_block_weights).
+void block_weight_sizes(const xema_block_cfg& cfg, int64_t bytes[12]);
+
+}  // namespace xema
+
+#ifdef __HIPCC__
+#include <hip/hip_runtime.h>
+namespace xema {
+// One block forward on stream s (arguments validated by the caller): x is
+// [B, L, D] in x_dtype (XEMA_BF16 or XEMA_F32), the arena follows `plan`,
+// out is [B, L, D] fp32.
+int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens, int x_dtype,
+              const xema_block_weights& w, const void* cond, int64_t ch, uint8_t* ws,
+              const xema_plan& plan, float* out, hipStream_t s);
+}  // namespace xema
+#endif
+
+namespace xema {
+
 }  // namespace xema

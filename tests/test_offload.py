@@ -1,0 +1,184 @@
+"""Selective weight offloading of an N-block step, without a GPU: the oracle
+plan against hand-worked cases and the properties Sec. 5.1 states (only as
+much as needed; offloaded blocks N/K apart), the fp64 step oracle against
+the scalar brute force, and the C++ planner against the oracle."""
+import numpy as np
+import pytest
+
+import paper_2607_11136_amd as X
+import workloads as W
+from oracle import brute
+from oracle import offload as OF
+from oracle import step as OS
+
+
+def _cfg(s):
+    return X.block_cfg(s.hidden, s.heads, s.head_dim, s.mlp_hidden, s.cond_dim, s.rope_dims,
+                       s.rope_theta, s.ln_eps, s.qk_eps)
+
+
+def _sizes(s):
+    return OF.block_weight_sizes(s.hidden, s.mlp_hidden, s.cond_dim, s.head_dim)
+
+
+# -- the oracle plan ----------------------------------------------------------------------
+
+
+def test_positions_hand_worked():
+    assert OF.offloaded_positions(4, 2) == [1, 3]
+    assert OF.offloaded_positions(5, 2) == [1, 4]
+    assert OF.offloaded_positions(3, 3) == [0, 1, 2]
+    assert OF.offloaded_positions(56, 16) == [2, 6, 9, 13, 16, 20, 23, 27, 30, 34, 37, 41, 44, 48, 51, 55]
+    assert OF.offloaded_positions(7, 0) == []
+
+
+@pytest.mark.parametrize("n", [1, 2, 5, 13, 28, 56, 256])
+def test_positions_are_spread_uniformly(n):
+    for k in range(1, n + 1):
+        pos = OF.offloaded_positions(n, k)
+        assert len(set(pos)) == k and pos == sorted(pos) and pos[-1] == n - 1 and pos[0] >= 0
+        gaps = np.diff([-1] + pos)
+        assert set(gaps.tolist()) <= {n // k, -(-n // k)}, (n, k, gaps)
+
+
+def test_slot_bytes_hand_worked():
+    # D = 256, F = 1024, D_c = 256, d = 64: every tensor but the gains is a
+    # multiple of 256 bytes; the 128-byte gains round up to 256
+    sizes = OF.block_weight_sizes(256, 1024, 256, 64)
+    assert sizes == [786432, 3072, 393216, 1536, 128, 128, 131072, 512, 524288, 2048, 524288, 512]
+    assert OF.slot_bytes(sizes) == sum(sizes) + 2 * 128
+
+
+def test_budget_plan_is_the_smallest_k_that_fits():
+    sizes = _sizes(W.IMAGE)
+    n, per = 28, sum(sizes)
+    slot = OF.slot_bytes(sizes)
+    for s_req in (1, 2, 3):
+        for budget in [n * per, n * per - 1, 20 * per, 10 * per + 7, 3 * slot, 2 * slot, slot, 0]:
+            p = OF.plan_for_budget(n, budget, s_req, sizes)
+            if p is None:
+                assert OF.plan(n, n, s_req, sizes)["device_weight_bytes"] > budget
+                continue
+            k = p["n_offloaded"]
+            assert p["device_weight_bytes"] <= budget
+            assert all(OF.plan(n, j, s_req, sizes)["device_weight_bytes"] > budget for j in range(k))
+    # every block resident when the budget holds them all: nothing offloaded
+    assert OF.plan_for_budget(n, n * per, 2, sizes)["n_offloaded"] == 0
+    # one block too many: offloading must also pay for its staging slots
+    p = OF.plan_for_budget(n, n * per - 1, 2, sizes)
+    assert p["n_offloaded"] == 3 and p["n_staging"] == 2
+
+
+# -- the step oracle -----------------------------------------------------------------------
+
+
+def _kw(s):
+    return dict(heads=s.heads, head_dim=s.head_dim, text_len=s.text_len, grid=s.grid,
+                rope_dims=s.rope_dims, rope_theta=s.rope_theta, ln_eps=s.ln_eps, qk_eps=s.qk_eps)
+
+
+def test_step_matches_scalar_brute_force_over_three_blocks():
+    s = W.tiny_shape()
+    inp = W.make_inputs(s)
+    ws = [{k: W.bf16_bits_to_f64(v) for k, v in w.items()} for w in W.step_weights(s, 3)]
+    x, c = inp.f64("x"), inp.f64("cond")
+    a = OS.step_forward(x, c, ws, **_kw(s))
+    b = x
+    for w in ws:
+        b = np.array(brute.block_forward(b.tolist(), c.tolist(), {k: v.tolist() for k, v in w.items()},
+                                         **_kw(s)))
+    assert np.max(np.abs(a - b)) / np.max(np.abs(b)) <= 1e-12
+
+
+def test_step_blocks_are_distinct_and_zero_gates_are_identity():
+    s = W.tiny_shape()
+    inp = W.make_inputs(s)
+    ws = [{k: W.bf16_bits_to_f64(v) for k, v in w.items()} for w in W.step_weights(s, 3)]
+    assert not np.array_equal(ws[0]["qkv_w"], ws[1]["qkv_w"])
+    D = s.hidden
+    for w in ws:
+        for blk in (2, 5):
+            w["ada_w"][blk * D:(blk + 1) * D] = 0.0
+            w["ada_b"][blk * D:(blk + 1) * D] = 0.0
+    x = inp.f64("x")
+    assert np.array_equal(OS.step_forward(x, inp.f64("cond"), ws, **_kw(s)), x)
+
+
+# -- the C++ planner against the oracle -----------------------------------------------------------
+
+
+def _same(p, ref, n):
+    assert p.n_blocks == n
+    assert p.n_offloaded == ref["n_offloaded"] and p.n_staging == ref["n_staging"]
+    assert p.offloaded_blocks() == ref["offloaded"]
+    for f in ("block_weight_bytes", "resident_weight_bytes", "staging_bytes", "device_weight_bytes"):
+        assert getattr(p, f) == ref[f], f
+
+
+@pytest.mark.parametrize("name", ["tiny", "image", "video", "long"])
+def test_cpp_plan_matches_oracle(name):
+    s = W.CONFIGS[name]
+    cfg, sizes = _cfg(s), _sizes(s)
+    for n in (1, 5, 28, 56):
+        for k in sorted({0, 1, n // 3, n // 2, n}):
+            for st in (1, 2, 4):
+                _same(X.xema_offload_plan_k(cfg, n, k, st), OF.plan(n, k, st, sizes), n)
+        per = sum(sizes)
+        for budget in (n * per, n * per - 1, (n // 2) * per, 3 * OF.slot_bytes(sizes), 100):
+            ref = OF.plan_for_budget(n, budget, 2, sizes)
+            if ref is None:
+                with pytest.raises(X.XemaError) as e:
+                    X.xema_offload_plan_budget(cfg, n, budget, 2)
+                assert e.value.status == X.XEMA_ERR_BUDGET_TOO_SMALL
+                _same(e.value.plan, OF.plan(n, n, 2, sizes), n)
+            else:
+                _same(X.xema_offload_plan_budget(cfg, n, budget, 2), ref, n)
+
+
+def test_step_workspace_is_arena_plus_residual_plus_staging():
+    s = W.VIDEO
+    cfg, req = _cfg(s), X.request(s.batch, s.text_len, *s.grid)
+    for k, st, chunk in ((0, 2, 0), (7, 2, 0), (7, 3, 4096), (28, 1, 0)):
+        p = X.xema_offload_plan_k(cfg, 28, k, st)
+        arena = X.xema_workspace_bytes(cfg, req, chunk)
+        resid = s.batch * s.seq_len * s.hidden * 4
+        expect = -(-arena // 256) * 256 + -(-resid // 256) * 256 + p.staging_bytes
+        assert X.xema_step_workspace_bytes(cfg, req, chunk, p) == expect
+
+
+def test_offload_errors():
+    cfg = _cfg(W.TINY)
+    lib = X.lib()
+    p = X.OffloadPlan()
+    import ctypes
+    assert lib.xema_offload_plan_k(ctypes.byref(cfg), 0, 0, 1, ctypes.byref(p)) == X.XEMA_ERR_INVALID_ARG
+    assert lib.xema_offload_plan_k(ctypes.byref(cfg), 4, 5, 1, ctypes.byref(p)) == X.XEMA_ERR_INVALID_ARG
+    assert lib.xema_offload_plan_k(ctypes.byref(cfg), 4, 2, 0, ctypes.byref(p)) == X.XEMA_ERR_INVALID_ARG
+    assert lib.xema_offload_plan_k(ctypes.byref(cfg), X.XEMA_MAX_BLOCKS + 1, 0, 1,
+                                   ctypes.byref(p)) == X.XEMA_ERR_INVALID_ARG
+    bad = X.block_cfg(256, 8, 32, 1024, 256, (8, 12, 12))
+    assert lib.xema_offload_plan_k(ctypes.byref(bad), 4, 2, 1, ctypes.byref(p)) == X.XEMA_ERR_UNSUPPORTED
+    # a plan the library did not make is refused
+    good = X.xema_offload_plan_k(cfg, 6, 2, 2)
+    req = X.request(1, W.TINY.text_len, *W.TINY.grid)
+    n = ctypes.c_int64()
+    tampered = X.xema_offload_plan_k(cfg, 6, 2, 2)
+    tampered.offloaded[0] = 1
+    assert lib.xema_step_workspace_bytes(ctypes.byref(cfg), ctypes.byref(req), 0, ctypes.byref(tampered),
+                                         ctypes.byref(n)) == X.XEMA_ERR_INVALID_ARG
+    assert lib.xema_step_workspace_bytes(ctypes.byref(cfg), ctypes.byref(req), 0, ctypes.byref(good),
+                                         ctypes.byref(n)) == X.XEMA_OK
+    # the step validates before touching the GPU
+    f = 1 << 20
+    w = (X.BlockWeights * 6)()
+    for i in range(6):
+        for name in X.WEIGHT_FIELDS:
+            setattr(w[i], name, f)
+    ws = n.value
+    assert lib.xema_dit_step_fwd(ctypes.byref(cfg), ctypes.byref(req), f, w, ctypes.byref(good), f, 0,
+                                 f * 64, ws - 256, f * 4096, None, None) == X.XEMA_ERR_WORKSPACE_TOO_SMALL
+    assert lib.xema_dit_step_fwd(ctypes.byref(cfg), ctypes.byref(req), f, w, ctypes.byref(tampered), f, 0,
+                                 f * 64, ws, f * 4096, None, None) == X.XEMA_ERR_INVALID_ARG
+    w[3].o_w = f + 8
+    assert lib.xema_dit_step_fwd(ctypes.byref(cfg), ctypes.byref(req), f, w, ctypes.byref(good), f, 0,
+                                 f * 64, ws, f * 4096, None, None) == X.XEMA_ERR_MISALIGNED

@@ -178,3 +178,13 @@ def sample_rows(shape: BlockShape, n: int, seed: int = 7) -> List[int]:
     pick = set(int(i) for i in g.choice(L, size=min(n, L), replace=False))
     pick.update({0, L - 1, max(shape.text_len - 1, 0), min(shape.text_len, L - 1)})
     return sorted(pick)
+
+
+def step_weights(shape: BlockShape, n_blocks: int) -> List[Dict[str, np.ndarray]]:
+    """Distinct seeded weights (bf16 bit patterns) for the blocks of an
+    n-block step: block 0 has the shape's own weights, block i > 0 those of
+    seed id 1000 + 64 * cfg_id + i."""
+    out = [make_inputs(shape).weights]
+    for i in range(1, n_blocks):
+        out.append(make_inputs(shape, seed_id=1000 + 64 * shape.cfg_id + i).weights)
+    return out
