@@ -121,6 +121,109 @@ def bench_gpu(args, shape):
     }
 
 
+def bench_step(args, shape):
+    """N-block step with selective weight offloading: N blocks with distinct
+    random weights, the plan's K offloaded blocks kept in pinned host memory
+    and prefetched on a copy stream.  Prints one JSON line."""
+    import torch
+
+    import paper_2607_11136_amd as X
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    n = args.step_blocks
+    cfg = X.block_cfg(shape.hidden, shape.heads, shape.head_dim, shape.mlp_hidden, shape.cond_dim,
+                      shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps)
+    req = X.request(shape.batch, shape.text_len, *shape.grid)
+    if args.weight_budget is not None:
+        plan = X.xema_offload_plan_budget(cfg, n, args.weight_budget, args.staging)
+    else:
+        plan = X.xema_offload_plan_k(cfg, n, args.offload, args.staging)
+    off = set(plan.offloaded_blocks())
+    g = torch.Generator(device=dev).manual_seed(2607)
+    shapes = shape.weight_shapes()
+
+    def rand(shp, std, mean=0.0):
+        return (torch.randn(shp, device=dev, generator=g) * std + mean).to(torch.bfloat16)
+
+    blocks, keep = [], []
+    for i in range(n):
+        w = {}
+        for name, shp in shapes.items():
+            if name in ("q_gamma", "k_gamma"):
+                t = rand(shp, 0.1, 1.0)
+            else:
+                t = rand(shp, 1.0 / shape.fan_in(name) ** 0.5)
+            if i in off:
+                h = torch.empty(t.shape, dtype=torch.bfloat16, pin_memory=True)
+                h.copy_(t)
+                t = h
+            w[name] = t
+        keep.append(w)
+        blocks.append(X.block_weights(w))
+    x = rand((shape.batch, shape.seq_len, shape.hidden), 1.0)
+    cond = rand((shape.batch, shape.cond_dim), 1.0)
+    nbytes = X.xema_step_workspace_bytes(cfg, req, 0, plan)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((shape.batch, shape.seq_len, shape.hidden), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    copy_stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+
+    def step():
+        X.xema_dit_step_fwd(cfg, req, x, blocks, plan, cond, 0, ws, nbytes, out, stream, copy_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    # host-to-device rate of one block's weights alone (pinned, copy stream)
+    h2d_gbs = None
+    if off:
+        hw = keep[min(off)]
+        dst = {k: torch.empty_like(v, device=dev) for k, v in hw.items()}
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(copy_stream):
+            c0.record(copy_stream)
+            for k, v in hw.items():
+                dst[k].copy_(v, non_blocking=True)
+            c1.record(copy_stream)
+        torch.cuda.synchronize()
+        h2d_gbs = plan.block_weight_bytes / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    flops = n * shape.flops()
+    result = {
+        "metric": "DiT denoising step ms (N blocks, selective weight offloading)",
+        "value": round(ms, 3),
+        "unit": "ms",
+        "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+        "ms_per_block": round(ms / n, 3),
+        "dtype": "f16/bf16",
+        "data": "synthetic (random N(0,1) tokens and conditioning, N(0,1/fan_in) weights per block)",
+        "config": {
+            "workload": WORKLOAD_TEXT[args.workload], "n_blocks": n,
+            "n_offloaded": plan.n_offloaded, "n_staging": plan.n_staging,
+            "offloaded_blocks": sorted(off), "weight_budget_bytes": args.weight_budget,
+            "block_weight_bytes": plan.block_weight_bytes,
+            "device_weight_bytes": plan.device_weight_bytes,
+            "h2d_bytes_per_step": plan.n_offloaded * plan.block_weight_bytes,
+            "h2d_block_GBps": None if h2d_gbs is None else round(h2d_gbs, 1),
+            "device_peak_bytes": int(torch.cuda.max_memory_allocated()),
+        },
+    }
+    print(json.dumps(result), flush=True)
+
+
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attention_video_hbm_traffic.md")
 TRAFFIC_SOURCES = ("paper_2607_11136_amd/csrc/k_attention.hip", "paper_2607_11136_amd/csrc/device_common.h",
                    "paper_2607_11136_amd/csrc/kernels.h")
@@ -209,6 +312,12 @@ def main():
                     help="activation budget (arena bytes); default per workload, 2 GiB for video")
     ap.add_argument("--chunk", type=int, default=None, help="chunk_tokens instead of the planned one")
     ap.add_argument("--cpu-rows", type=int, default=3072)
+    ap.add_argument("--step-blocks", type=int, default=0,
+                    help="measure an N-block step with selective weight offloading instead")
+    ap.add_argument("--offload", type=int, default=0, help="offloaded blocks K (step mode)")
+    ap.add_argument("--weight-budget", type=int, default=None,
+                    help="device weight budget in bytes; the plan picks the smallest K (step mode)")
+    ap.add_argument("--staging", type=int, default=2, help="device staging slots (step mode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="also run a plain device copy of this size (calibrates HBM byte counters)")
@@ -225,6 +334,9 @@ def main():
 
     import workloads as W
     shape = W.CONFIGS[args.workload]
+    if args.step_blocks > 0:
+        bench_step(args, shape)
+        return
     if args.budget is None:
         args.budget = DEFAULT_BUDGET[args.workload]
     g = bench_gpu(args, shape)
