@@ -58,9 +58,15 @@ def bench_gpu(args, shape):
                       shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps)
     req = X.request(shape.batch, shape.text_len, *shape.grid)
     if args.chunk is not None:
-        plan = X.xema_workspace_layout(cfg, req, args.chunk)
+        group = args.batch_group or shape.batch
+        plan = X.xema_workspace_layout(cfg, X.request(min(group, shape.batch), shape.text_len, *shape.grid),
+                                       args.chunk)
+    elif args.batch_group:
+        group = args.batch_group
+        plan = X.xema_workspace_plan(cfg, X.request(group, shape.text_len, *shape.grid), args.budget)
     else:
-        plan = X.xema_workspace_plan(cfg, req, args.budget)
+        # chunking and temporary serialization, only as much as the budget needs
+        group, plan = X.xema_workspace_plan_serial(cfg, req, args.budget)
     ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=dev)
     out = torch.empty((shape.batch, shape.seq_len, shape.hidden), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -68,7 +74,8 @@ def bench_gpu(args, shape):
     torch.cuda.reset_peak_memory_stats()
 
     def step():
-        X.xema_dit_block_fwd(cfg, req, x, weights, cond, plan.chunk_tokens, ws, ws.numel(), out, stream)
+        X.xema_dit_block_fwd_serial(cfg, req, x, weights, cond, group, plan.chunk_tokens, ws, ws.numel(), out,
+                                    stream)
 
     for _ in range(args.warmup):
         step()
@@ -84,7 +91,8 @@ def bench_gpu(args, shape):
     print(f"[bench] block step: {ms:.3f} ms over {args.steps} steps", file=sys.stderr, flush=True)
 
     # dominant kernel: attention over all queries, on the Q/K/V^T the block left in the arena
-    B, H, L, d = shape.batch, shape.heads, shape.seq_len, shape.head_dim
+    # (which holds the sequences of one group when the batch runs in groups)
+    B, H, L, d = min(group, shape.batch), shape.heads, shape.seq_len, shape.head_dim
     Lp = X.padded_len(L)
     slots = plan.slots()
     o = torch.empty((B * L, H * d), dtype=torch.float16, device=dev)
@@ -117,6 +125,7 @@ def bench_gpu(args, shape):
         "ms": ms,
         "attn_ms": attn_ms,
         "plan": plan,
+        "batch_group": group,
         "device_peak_bytes": int(torch.cuda.max_memory_allocated()),
     }
 
@@ -311,6 +320,8 @@ def main():
     ap.add_argument("--budget", type=int, default=None,
                     help="activation budget (arena bytes); default per workload, 2 GiB for video")
     ap.add_argument("--chunk", type=int, default=None, help="chunk_tokens instead of the planned one")
+    ap.add_argument("--batch-group", type=int, default=None,
+                    help="sequences per group (temporary serialization) instead of the planned one")
     ap.add_argument("--cpu-rows", type=int, default=3072)
     ap.add_argument("--step-blocks", type=int, default=0,
                     help="measure an N-block step with selective weight offloading instead")
@@ -343,7 +354,7 @@ def main():
     flops = shape.flops()
     tflops = flops / (g["ms"] * 1e-3) / 1e12
     B, H, L, d = shape.batch, shape.heads, shape.seq_len, shape.head_dim
-    af = attention_flops(B, H, L, d)
+    af = attention_flops(min(g["batch_group"], B), H, L, d)
     attn_tflops = af / (g["attn_ms"] * 1e-3) / 1e12
     plan = g["plan"]
     result = {
@@ -364,12 +375,12 @@ def main():
             "workload": WORKLOAD_TEXT[args.workload],
             "batch": B, "seq_len": L, "hidden": shape.hidden, "heads": H, "head_dim": d,
             "mlp_hidden": shape.mlp_hidden, "flops_per_step": flops,
-            "budget_bytes": args.budget, "chunk_tokens": plan.chunk_tokens,
+            "budget_bytes": args.budget, "chunk_tokens": plan.chunk_tokens, "batch_group": g["batch_group"],
             "arena_bytes": plan.workspace_bytes, "device_peak_bytes": g["device_peak_bytes"],
         },
         "roofline": {
             "kernel": (f"{'k_attention_lazy<64>' if d == 64 else 'k_attention<128>'} (joint attention, "
-                       f"all {L} queries x {L} keys x {B * H} batch-heads)"),
+                       f"all {L} queries x {L} keys x {min(g['batch_group'], B) * H} batch-heads)"),
             "bound": "mfma",
             "achieved": round(attn_tflops, 2),
             "peak": PEAK_TFLOPS,

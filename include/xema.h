@@ -184,6 +184,35 @@ XEMA_API int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* r
                        void* workspace, int64_t workspace_bytes,
                        void* out, void* stream);
 
+/* Temporary serialization (Sec. 5.2, "Temporary serialization") together
+ * with chunking: a batch whose arena exceeds the budget can run its
+ * sequences through the block in equal groups of g < batch (g divides the
+ * batch), one group after another, each group seeing the arena of a
+ * g-sequence request; elsewhere the batch keeps its size.  Among the
+ * (g, chunk) pairs whose arena fits budget_bytes the plan takes the most
+ * tokens per launch (g * chunk), then the larger g: a proxy for the least
+ * latency overhead of pi* (Sec. 5.1), since launches over more tokens fill
+ * the GPU better.  With an ample budget it is (batch, L): no mitigation.
+ * *batch_group receives g and `out` the layout for a g-sequence request.
+ * Host only.
+ * Errors: as xema_workspace_plan; BUDGET_TOO_SMALL when even one sequence at
+ * the smallest chunk does not fit (out->min_workspace_bytes then holds that
+ * arena, *batch_group is 0).                                              */
+XEMA_API int xema_workspace_plan_serial(const xema_block_cfg* cfg, const xema_request* req,
+                               int64_t budget_bytes, int32_t* batch_group, xema_plan* out);
+
+/* xema_dit_block_fwd with the batch run in groups of batch_group sequences
+ * (1 <= batch_group; >= batch means one group).  The workspace needs the
+ * arena of a batch_group-sequence request and of the shorter last group
+ * (xema_workspace_plan_serial reports the larger).  The output is
+ * bit-identical for every batch_group and chunk_tokens.  Errors as
+ * xema_dit_block_fwd.                                                     */
+XEMA_API int xema_dit_block_fwd_serial(const xema_block_cfg* cfg, const xema_request* req,
+                              const void* tokens, const xema_block_weights* weights,
+                              const void* cond, int32_t batch_group, int32_t chunk_tokens,
+                              void* workspace, int64_t workspace_bytes,
+                              void* out, void* stream);
+
 /* Static string naming a status code. */
 XEMA_API const char* xema_status_str(int status);
 

@@ -160,3 +160,24 @@ def plan(shape, budget_bytes: int):
         if ws <= budget_bytes:
             return c, ws, smallest
     return None, None, smallest
+
+
+def plan_serial(shape, budget_bytes: int):
+    """Temporary serialization (Sec. 5.2) together with chunking, choosing
+    the mitigation with the least latency overhead (Sec. 5.1, pi*) by a
+    proxy: among the (g, c) whose arena fits `budget_bytes` (the batch split
+    into equal groups of g sequences run through the block one after
+    another, each in chunks of c tokens), the most tokens per launch g * c,
+    then the larger g.  Returns (g, chunk, arena bytes) or None."""
+    B = shape.batch
+    best = None
+    for g in range(B, 0, -1):
+        if B % g:
+            continue
+        for c in chunk_candidates(shape.seq_len):
+            need = workspace_bytes(shape.with_(batch=g), c)
+            if need <= budget_bytes:
+                if best is None or g * c > best[0] * best[1]:
+                    best = (g, c, need)
+                break
+    return best

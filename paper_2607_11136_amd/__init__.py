@@ -130,6 +130,11 @@ _SIGNATURES = {
                                             _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "xema_op_attention": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _P, _P]),
     "xema_op_convert_f16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "xema_workspace_plan_serial": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request),
+                                                  _I64, ctypes.POINTER(_I32), ctypes.POINTER(Plan)]),
+    "xema_dit_block_fwd_serial": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
+                                                 ctypes.POINTER(BlockWeights), _P, _I32, _I32, _P, _I64,
+                                                 _P, _P]),
     "xema_offload_plan_k": (ctypes.c_int, [ctypes.POINTER(BlockCfg), _I32, _I32, _I32,
                                            ctypes.POINTER(OffloadPlan)]),
     "xema_offload_plan_budget": (ctypes.c_int, [ctypes.POINTER(BlockCfg), _I32, _I64, _I32,
@@ -268,6 +273,30 @@ def xema_dit_block_fwd(cfg: BlockCfg, req: Request, tokens, weights: BlockWeight
                                     ctypes.byref(weights), _ptr(cond), chunk_tokens,
                                     _ptr(workspace), int(workspace_bytes), _ptr(out),
                                     _stream(stream)), "xema_dit_block_fwd")
+
+
+def xema_workspace_plan_serial(cfg: BlockCfg, req: Request, budget_bytes: int):
+    """(batch_group, plan): temporary serialization only when chunking alone
+    cannot fit the budget.  Raises XemaError (XEMA_ERR_BUDGET_TOO_SMALL, the
+    plan with min_workspace_bytes as `.plan`)."""
+    p = Plan()
+    g = _I32()
+    st = lib().xema_workspace_plan_serial(ctypes.byref(cfg), ctypes.byref(req), int(budget_bytes),
+                                          ctypes.byref(g), ctypes.byref(p))
+    if st != XEMA_OK:
+        e = XemaError(st, "xema_workspace_plan_serial")
+        e.plan = p
+        raise e
+    return g.value, p
+
+
+def xema_dit_block_fwd_serial(cfg: BlockCfg, req: Request, tokens, weights: BlockWeights, cond,
+                              batch_group: int, chunk_tokens: int, workspace, workspace_bytes: int, out,
+                              stream=None) -> None:
+    _check(lib().xema_dit_block_fwd_serial(ctypes.byref(cfg), ctypes.byref(req), _ptr(tokens),
+                                           ctypes.byref(weights), _ptr(cond), batch_group, chunk_tokens,
+                                           _ptr(workspace), int(workspace_bytes), _ptr(out),
+                                           _stream(stream)), "xema_dit_block_fwd_serial")
 
 
 def xema_op_adaln(cond, w, bias, batch: int, cond_dim: int, out_dim: int, mod, stream=None) -> None:

@@ -308,10 +308,11 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
 }  // namespace xema
 
 
-extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
-                                  const void* tokens, const xema_block_weights* w,
-                                  const void* cond, int32_t chunk_tokens, void* workspace,
-                                  int64_t workspace_bytes, void* out, void* stream) {
+// Validation shared by the block entry points: everything but the arena
+// size, which depends on the group size.
+static int check_block_call(const xema_block_cfg* cfg, const xema_request* req, const void* tokens,
+                            const xema_block_weights* w, const void* cond, void* workspace,
+                            int64_t workspace_bytes, void* out) {
   int st = validate_shapes(cfg, req);
   if (st != XEMA_OK) return st;
   if (!tokens || !w || !cond || !workspace || !out || workspace_bytes <= 0)
@@ -344,13 +345,47 @@ extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request*
     return XEMA_ERR_INVALID_ARG;
   for (int i = 0; i < 12; ++i)
     if (overlaps(workspace, workspace_bytes, wp[i], wbytes[i])) return XEMA_ERR_INVALID_ARG;
-
-  const int64_t ch = effective_chunk(L, chunk_tokens);
-  xema_plan plan;
-  st = layout_for_chunk(c, r, ch, &plan);
-  if (st != XEMA_OK) return st;
-  if (workspace_bytes < plan.workspace_bytes) return XEMA_ERR_WORKSPACE_TOO_SMALL;
-  return run_block(c, r, tokens, XEMA_BF16, *w, cond, ch, (uint8_t*)workspace, plan, (float*)out,
-                   (hipStream_t)stream);
+  return XEMA_OK;
 }
 
+extern "C" int xema_dit_block_fwd_serial(const xema_block_cfg* cfg, const xema_request* req,
+                                         const void* tokens, const xema_block_weights* w,
+                                         const void* cond, int32_t batch_group,
+                                         int32_t chunk_tokens, void* workspace,
+                                         int64_t workspace_bytes, void* out, void* stream) {
+  int st = check_block_call(cfg, req, tokens, w, cond, workspace, workspace_bytes, out);
+  if (st != XEMA_OK) return st;
+  if (batch_group < 1) return XEMA_ERR_INVALID_ARG;
+  const xema_block_cfg& c = *cfg;
+  const int64_t B = req->batch, L = seq_len(*req), D = c.hidden, Dc = c.cond_dim;
+  const int64_t g = std::min<int64_t>(batch_group, B);
+  const int64_t ch = effective_chunk(L, chunk_tokens);
+  // groups of g sequences, one after another; a shorter last group runs with
+  // the layout of its own request.  Both layouts are checked before any launch.
+  xema_request rg = *req, rl = *req;
+  rg.batch = (int32_t)g;
+  rl.batch = (int32_t)(B % g == 0 ? g : B % g);
+  xema_plan plan_g, plan_l;
+  st = layout_for_chunk(c, rg, ch, &plan_g);
+  if (st != XEMA_OK) return st;
+  st = layout_for_chunk(c, rl, ch, &plan_l);
+  if (st != XEMA_OK) return st;
+  if (workspace_bytes < plan_g.workspace_bytes || workspace_bytes < plan_l.workspace_bytes)
+    return XEMA_ERR_WORKSPACE_TOO_SMALL;
+  for (int64_t b0 = 0; b0 < B; b0 += g) {
+    const bool last = b0 + g >= B;
+    st = run_block(c, last ? rl : rg, (const uint16_t*)tokens + b0 * L * D, XEMA_BF16, *w,
+                   (const uint16_t*)cond + b0 * Dc, ch, (uint8_t*)workspace, last ? plan_l : plan_g,
+                   (float*)out + b0 * L * D, (hipStream_t)stream);
+    if (st != XEMA_OK) return st;
+  }
+  return XEMA_OK;
+}
+
+extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
+                                  const void* tokens, const xema_block_weights* w,
+                                  const void* cond, int32_t chunk_tokens, void* workspace,
+                                  int64_t workspace_bytes, void* out, void* stream) {
+  return xema_dit_block_fwd_serial(cfg, req, tokens, w, cond, req ? req->batch : 1, chunk_tokens,
+                                   workspace, workspace_bytes, out, stream);
+}

@@ -212,6 +212,50 @@ extern "C" int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request
   return XEMA_ERR_BUDGET_TOO_SMALL;
 }
 
+extern "C" int xema_workspace_plan_serial(const xema_block_cfg* cfg, const xema_request* req,
+                                          int64_t budget_bytes, int32_t* batch_group,
+                                          xema_plan* out) {
+  if (!out || !batch_group) return XEMA_ERR_INVALID_ARG;
+  const int st = validate_shapes(cfg, req);
+  if (st != XEMA_OK) return st;
+  *batch_group = 0;
+  const int64_t L = seq_len(*req);
+  std::vector<int64_t> cands{L};
+  for (int64_t c = (L - 1) / XEMA_CHUNK_GRANULE * XEMA_CHUNK_GRANULE; c > 0; c -= XEMA_CHUNK_GRANULE)
+    cands.push_back(c);
+  // Among the (g, c) whose arena fits, the most tokens per launch (g * c),
+  // then the larger group: the launches that fill the GPU best.  With the
+  // budget ample this is (batch, L), no mitigation at all.
+  int64_t best_tokens = 0;
+  for (int32_t g = req->batch; g >= 1; --g) {
+    if (req->batch % g) continue;  // equal groups only
+    xema_request rg = *req;
+    rg.batch = g;
+    for (int64_t c : cands) {
+      if ((int64_t)g * c <= best_tokens) break;  // candidates shrink: nothing better below
+      xema_plan pg;
+      layout_for_chunk(*cfg, rg, c, &pg);
+      if (pg.workspace_bytes <= budget_bytes) {
+        *out = pg;
+        *batch_group = g;
+        best_tokens = (int64_t)g * c;
+        break;  // the largest fitting chunk for this g
+      }
+    }
+  }
+  xema_request r1 = *req;
+  r1.batch = 1;
+  xema_plan smallest;
+  layout_for_chunk(*cfg, r1, cands.back(), &smallest);
+  if (*batch_group == 0) {
+    std::memset(out, 0, sizeof(*out));
+    out->min_workspace_bytes = smallest.workspace_bytes;
+    return XEMA_ERR_BUDGET_TOO_SMALL;
+  }
+  out->min_workspace_bytes = smallest.workspace_bytes;
+  return XEMA_OK;
+}
+
 extern "C" const char* xema_status_str(int status) {
   switch (status) {
     case XEMA_OK: return "ok";

@@ -35,7 +35,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = X.lib()
     declared = _declared_symbols()
-    assert len(declared) == 17, declared
+    assert len(declared) == 19, declared
     for name in declared:
         assert hasattr(lib, name), name
     assert declared == set(X.EXPORTED)
@@ -91,6 +91,33 @@ def test_highres_32gb_budget_runs_unchunked():
     p = X.xema_workspace_plan(_cfg(s), _req(s), 32 * 2**30)
     assert p.chunk_tokens == s.seq_len
     assert p.workspace_bytes <= 32 * 2**30
+
+
+@pytest.mark.parametrize("name", ["image_b4", "long", "tiny"])
+def test_serial_plan_matches_oracle(name):
+    """Temporary serialization: the largest group size, then the largest
+    chunk, that fits; only when chunking alone cannot fit the whole batch."""
+    s = W.CONFIGS[name]
+    cfg, req = _cfg(s), _req(s)
+    full_min = OL.workspace_bytes(s, OL.chunk_candidates(s.seq_len)[-1])
+    one = s.with_(batch=1)
+    one_min = OL.workspace_bytes(one, OL.chunk_candidates(s.seq_len)[-1])
+    budgets = [OL.workspace_bytes(s, 0), full_min, full_min - 1, (full_min + one_min) // 2, one_min, one_min - 1]
+    for budget in budgets:
+        ref = OL.plan_serial(s, budget)
+        if ref is None:
+            with pytest.raises(X.XemaError) as e:
+                X.xema_workspace_plan_serial(cfg, req, budget)
+            assert e.value.status == X.XEMA_ERR_BUDGET_TOO_SMALL
+            assert e.value.plan.min_workspace_bytes == one_min
+            continue
+        g, p = X.xema_workspace_plan_serial(cfg, req, budget)
+        assert (g, p.chunk_tokens, p.workspace_bytes) == ref, (budget, ref)
+        assert p.workspace_bytes <= budget
+        if budget >= OL.workspace_bytes(s, 0):
+            assert (g, p.chunk_tokens) == (s.batch, s.seq_len)   # no mitigation at all
+        if budget < full_min:
+            assert g < s.batch   # chunking alone cannot fit the whole batch
 
 
 @pytest.mark.parametrize("hwt,grid", [((1024, 1024, 1), (1, 64, 64)), ((480, 720, 49), (13, 30, 45)),

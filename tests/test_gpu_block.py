@@ -165,6 +165,40 @@ def test_budget_plan_drives_the_call():
     assert e.value.status == X.XEMA_ERR_WORKSPACE_TOO_SMALL
 
 
+def test_temporary_serialization_is_bit_identical():
+    """Sequences run through the block in groups (temporary serialization):
+    every group size and chunk gives the unserialized output bit for bit."""
+    s = SMALL["d128_b3"]
+    dev = _device(s)
+    base, _, _ = dev.run(0)
+    for g, chunk in ((1, 0), (2, 0), (2, 100), (1, 37), (5, 64)):
+        sub = X.request(min(g, s.batch), s.text_len, *s.grid)
+        r_last = X.request(s.batch % g or min(g, s.batch), s.text_len, *s.grid)
+        nbytes = max(X.xema_workspace_bytes(dev.cfg, sub, chunk), X.xema_workspace_bytes(dev.cfg, r_last, chunk))
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+        out = torch.empty_like(base)
+        X.xema_dit_block_fwd_serial(dev.cfg, dev.req, dev.x, dev.weights, dev.cond, g, chunk, ws, nbytes, out)
+        torch.cuda.synchronize()
+        assert torch.equal(out, base), (g, chunk)
+
+
+def test_serial_plan_drives_the_call_below_the_batch_minimum():
+    """A budget below the whole batch's smallest arena: the plan serializes,
+    and the call with the planned group and chunk reproduces the output."""
+    s = SMALL["d128_b3"]
+    dev = _device(s)
+    base, _, _ = dev.run(0)
+    full_min = X.xema_workspace_layout(dev.cfg, dev.req, 0).min_workspace_bytes
+    g, plan = X.xema_workspace_plan_serial(dev.cfg, dev.req, full_min - 1)
+    assert g < s.batch and plan.workspace_bytes <= full_min - 1
+    ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+    out = torch.empty_like(base)
+    X.xema_dit_block_fwd_serial(dev.cfg, dev.req, dev.x, dev.weights, dev.cond, g, plan.chunk_tokens, ws,
+                                ws.numel(), out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, base)
+
+
 # -- the five workloads at full size, on sampled rows ---------------------------------
 
 FULL = [("tiny", 0, None), ("image", 0, 48), ("image_b4", 0, 24), ("video", 0, 48),
