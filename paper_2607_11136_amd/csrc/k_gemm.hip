@@ -64,7 +64,7 @@ constexpr int NS = 4;                      // LDS pipeline stages
 constexpr int B_BYTES = BN * BK * 2;       // 16 KiB of B per stage
 constexpr int GROUP_M = 8;
 constexpr int NWAVES = 8;                  // 2 x 4 waves, two per SIMD
-constexpr int WN = 64;                     // output columns per wave
+constexpr int WN = BN * 2 / NWAVES;        // output columns per wave (64)
 constexpr int NJ = WN / 32;                // 32-column MFMA blocks per wave
 constexpr int BUF_FLAGS = 0x00020000;      // raw buffer, 32-bit dwords
 
@@ -138,7 +138,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   constexpr int MI = BM / 64;                         // 32-row MFMA blocks per wave
   constexpr int A_BYTES = BM * BK * 2;
   constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-  constexpr int A_LOADS = BM / 128, B_LOADS = BN / 128;  // 1 KiB loads per wave per stage
+  constexpr int A_LOADS = BM / NWAVES / 16, B_LOADS = BN / NWAVES / 16;  // 1 KiB loads per wave per stage
   constexpr int LPS = A_LOADS + B_LOADS;
   typedef typename Mfma<T>::frag frag;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][STAGE_BYTES];
@@ -184,19 +184,22 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   // A step past the last one is issued at an offset beyond the descriptor's
   // range: the hardware moves no data (the lanes read as zero) and the loop
   // body stays free of branches, so its loads can be spread between MFMAs.
+  // (The out-of-range bit is ORed in arithmetically: a select here is turned
+  // into branches around each load, which keeps the loads out of the MFMA
+  // block.  Tile offsets stay below 2^31, checked by the host.)
   auto issue = [&](int kt) {
     uint8_t* st = smem[kt % NS];
-    const bool valid = kt < KT;
+    const uint32_t oob = (uint32_t)((KT - 1 - kt) >> 31) << 31;  // 0x80000000 once kt >= KT
     const uint32_t kbyte = (uint32_t)(kt * BK * 2);
 #pragma unroll
     for (int c = 0; c < A_LOADS; ++c) {
-      const uint32_t off = valid ? a_off + c * chunk_stride + kbyte : 0x80000000u;
+      const uint32_t off = (a_off + c * chunk_stride + kbyte) | oob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * A_LOADS + c) * 1024), 16,
                                                off, 0, 0, 0);
     }
 #pragma unroll
     for (int c = 0; c < B_LOADS; ++c) {
-      const uint32_t off = valid ? b_off + c * chunk_stride + kbyte : 0x80000000u;
+      const uint32_t off = (b_off + c * chunk_stride + kbyte) | oob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rb, (lds_ptr_t)(st + A_BYTES + (wave * B_LOADS + c) * 1024), 16, off, 0, 0, 0);
     }
