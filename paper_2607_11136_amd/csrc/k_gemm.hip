@@ -2,12 +2,13 @@
 // (bias, bias + GELU-tanh, gated residual).  Steps a2, a5, a7, a8.
 //
 // Tiling: a BM x 256 output tile per workgroup (BM = 256 or 128), K in steps
-// of 32.  Eight waves (two per SIMD) in a 2 x 4 grid each own a (BM/2) x 64
+// of 64.  Eight waves (two per SIMD) in a 2 x 4 grid each own a (BM/2) x 64
 // sub-tile held as (BM/64) x 2 accumulators of v_mfma_f32_32x32x16.  Operand
 // tiles go from HBM straight into LDS with buffer_load ... lds (no VGPR
-// staging) through a ring of four stages, so up to three K-steps of loads are
-// in flight while one is consumed: a step's loads have about two steps of
-// MFMA work to land, which covers the latency of L2 misses.  The buffer
+// staging) through two stages: the loads of step k+1 are issued as step k
+// starts and have three of its four MFMA k-steps to land.  Wide steps halve
+// the barriers and give 128-byte row segments (whole cache lines) per load,
+// which measured faster than a four-deep ring of 32-wide steps.  The buffer
 // descriptor of each tile covers only that tile's rows, so rows past M read
 // as zero.
 //
@@ -17,9 +18,9 @@
 // 840 tiles of 256 x 256 = 3.3 waves; 64 tile-rows of 256 plus 11 of 128 fill
 // 3 waves and half a wave of half-size tiles).
 //
-// LDS layout: a stage holds BM rows of A and 256 rows of B, 32 elements (64
-// bytes = four 16-byte slots) each; slot j of row r is stored at slot
-// j ^ ((r >> 2) & 3).  The LDS has 64 four-byte banks and serves a 16-byte
+// LDS layout: a stage holds BM rows of A and 256 rows of B, 64 elements (128
+// bytes = eight 16-byte slots) each; slot j of row r is stored at slot
+// j ^ ((r >> 1) & 7).  The LDS has 64 four-byte banks and serves a 16-byte
 // read for 16 lanes per cycle; those 16 lanes read 16 consecutive rows at
 // one logical slot, and the swizzle spreads them over all 64 banks.
 //
@@ -31,8 +32,8 @@
 // below gives each XCD a contiguous range of tiles, walked in groups of 8
 // tile-rows, so tiles that share operand panels share an L2.
 //
-// Determinism: every output element is the sum over ascending 32-wide K
-// steps, each reduced by the same MFMA sequence, whatever M, BM, the row maps
+// Determinism: every output element is the sum over ascending 16-wide K
+// steps, one MFMA each, in the same sequence whatever M, BM, the row maps
 // or the tile position are; so chunked and unchunked calls, and either tile
 // height, agree bit for bit.
 #include "device_common.h"
@@ -59,12 +60,18 @@ struct Mfma<f16> {
   }
 };
 
-constexpr int BN = 256, BK = 32;
-constexpr int NS = 4;                      // LDS pipeline stages
-constexpr int B_BYTES = BN * BK * 2;       // 16 KiB of B per stage
+constexpr int BN = 256, BK = 64;
+constexpr int KS = BK / 16;                // MFMA k-steps per stage
+constexpr int ROWB = BK * 2;               // bytes of one operand row in a stage
+constexpr int SLOTS = BK / 8;              // 16-byte slots per row
+constexpr int RPL = 1024 / ROWB;           // rows filled by one 1 KiB wave load
+constexpr int NS = 2;                      // LDS pipeline stages
+constexpr int B_BYTES = BN * BK * 2;       // B bytes per stage
 constexpr int GROUP_M = 8;
 constexpr int NWAVES = 8;                  // 2 x 4 waves, two per SIMD
-constexpr int WN = BN * 2 / NWAVES;        // output columns per wave (64)
+constexpr int WN = BN * 2 / NWAVES;        // output columns per wave
+// slot swizzle of a 128-byte row (two rows share a 256-byte bank line)
+__host__ __device__ constexpr int row_swz(int r) { return (r >> 1) & 7; }
 constexpr int NJ = WN / 32;                // 32-column MFMA blocks per wave
 constexpr int BUF_FLAGS = 0x00020000;      // raw buffer, 32-bit dwords
 
@@ -113,6 +120,7 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); 
 template <int LOADS_PER_STAGE>
 __device__ __forceinline__ void stage_barrier(int stages_after) {
   static_assert(2 * LOADS_PER_STAGE < 64, "vmcnt range");
+  static_assert(NS >= 2 && NS <= 4, "at most two stages in flight after the next");
   __builtin_amdgcn_sched_barrier(0);
   if (stages_after >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS_PER_STAGE));
   else if (stages_after == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS_PER_STAGE));
@@ -133,12 +141,12 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
                                                  const uint16_t* __restrict__ bias,
                                                  CT* __restrict__ cout, const RT* __restrict__ resid,
                                                  const float* __restrict__ gate) {
-  static_assert(NS == 4, "stage_barrier assumes at most two stages in flight after the next");
   static_assert(BM == 256 || BM == 128, "tile heights");
   constexpr int MI = BM / 64;                         // 32-row MFMA blocks per wave
   constexpr int A_BYTES = BM * BK * 2;
   constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-  constexpr int A_LOADS = BM / NWAVES / 16, B_LOADS = BN / NWAVES / 16;  // 1 KiB loads per wave per stage
+  constexpr int A_LOADS = BM / NWAVES / RPL, B_LOADS = BN / NWAVES / RPL;  // 1 KiB loads per wave per stage
+  static_assert(A_LOADS * NWAVES * RPL == BM && B_LOADS * NWAVES * RPL == BN, "load split");
   constexpr int LPS = A_LOADS + B_LOADS;
   typedef typename Mfma<T>::frag frag;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][STAGE_BYTES];
@@ -171,15 +179,23 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * K, rows_a * K * 2);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bw + (int64_t)n0 * K, (int64_t)BN * K * 2);
 
-  // Direct-to-LDS load plan: a 1 KiB wave instruction fills 16 rows; wave w
-  // fills rows (BM/8) w .. of A and 32 w .. 32 w + 31 of B.  Lane l writes
-  // row 16c + l/4 of its chunk at physical slot l%4, so it fetches logical
-  // slot (l%4) ^ ((l >> 4) & 3).  The whole offset is in the VGPR operand,
-  // which is what the buffer range check covers (rows past M read as zero).
-  const uint32_t lane_off = (uint32_t)(((lane >> 2) * K + (((lane & 3) ^ ((lane >> 4) & 3)) * 8)) * 2);
-  const uint32_t a_off = lane_off + (uint32_t)(wave * A_LOADS * 16 * K * 2);
-  const uint32_t b_off = lane_off + (uint32_t)(wave * B_LOADS * 16 * K * 2);
-  const uint32_t chunk_stride = (uint32_t)(16 * K * 2);
+  // Direct-to-LDS load plan: a 1 KiB wave instruction fills RPL rows; wave w
+  // fills A rows (BM/NWAVES) w .. and B rows (BN/NWAVES) w ..  Lane l writes
+  // row l / SLOTS of its chunk at physical slot l % SLOTS, so it fetches the
+  // logical slot that the row's swizzle maps there.  The whole offset is in
+  // the VGPR operand, which is what the buffer range check covers (rows past
+  // M read as zero).
+  uint32_t a_off[A_LOADS], b_off[B_LOADS];
+#pragma unroll
+  for (int c = 0; c < A_LOADS; ++c) {
+    const int row = (wave * A_LOADS + c) * RPL + lane / SLOTS;
+    a_off[c] = (uint32_t)((row * K + (((lane % SLOTS) ^ row_swz(row)) * 8)) * 2);
+  }
+#pragma unroll
+  for (int c = 0; c < B_LOADS; ++c) {
+    const int row = (wave * B_LOADS + c) * RPL + lane / SLOTS;
+    b_off[c] = (uint32_t)((row * K + (((lane % SLOTS) ^ row_swz(row)) * 8)) * 2);
+  }
 
   // A step past the last one is issued at an offset beyond the descriptor's
   // range: the hardware moves no data (the lanes read as zero) and the loop
@@ -193,13 +209,13 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
     const uint32_t kbyte = (uint32_t)(kt * BK * 2);
 #pragma unroll
     for (int c = 0; c < A_LOADS; ++c) {
-      const uint32_t off = (a_off + c * chunk_stride + kbyte) | oob;
+      const uint32_t off = (a_off[c] + kbyte) | oob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * A_LOADS + c) * 1024), 16,
                                                off, 0, 0, 0);
     }
 #pragma unroll
     for (int c = 0; c < B_LOADS; ++c) {
-      const uint32_t off = (b_off + c * chunk_stride + kbyte) | oob;
+      const uint32_t off = (b_off[c] + kbyte) | oob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rb, (lds_ptr_t)(st + A_BYTES + (wave * B_LOADS + c) * 1024), 16, off, 0, 0, 0);
     }
@@ -214,19 +230,20 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // fragment addressing: lane reads row (block + lane%32), k-slot kk*2 + lane/32
-  const int r32 = lane & 31, hi = lane >> 5, sw = (lane >> 2) & 3;
-  const int a_row0 = (wm * (BM / 2) + r32) * 64;  // byte offset of this lane's first A row
-  const int b_row0 = (wn * WN + r32) * 64;
+  // (blocks start at multiples of 32 rows, so the swizzle is the lane's own)
+  const int r32 = lane & 31, hi = lane >> 5, sw = row_swz(r32);
+  const int a_row0 = (wm * (BM / 2) + r32) * ROWB;  // byte offset of this lane's first A row
+  const int b_row0 = (wn * WN + r32) * ROWB;
 
   frag fx[2][MI], fw[2][NJ];
   auto read_frags = [&](const uint8_t* st, int kk, frag (&x)[MI], frag (&wv)[NJ]) {
     const int so = (((kk * 2 + hi) ^ sw) * 16);
 #pragma unroll
     for (int i = 0; i < MI; ++i)
-      x[i] = *reinterpret_cast<const frag*>(st + a_row0 + i * 32 * 64 + so);
+      x[i] = *reinterpret_cast<const frag*>(st + a_row0 + i * 32 * ROWB + so);
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
-      wv[j] = *reinterpret_cast<const frag*>(st + A_BYTES + b_row0 + j * 32 * 64 + so);
+      wv[j] = *reinterpret_cast<const frag*>(st + A_BYTES + b_row0 + j * 32 * ROWB + so);
   };
   auto mfma_step = [&](const frag (&x)[MI], const frag (&wv)[NJ]) {
 #pragma unroll
@@ -242,26 +259,30 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   read_frags(smem[0], 0, fx[0], fw[0]);
   for (int kt = 0; kt < KT; ++kt) {
     // The stage refilled here was consumed at step kt-1, and every wave has
-    // passed the barrier that ended step kt-1.  K-step 0 of this stage runs
-    // with the loads of step kt+NS-1 and the fragments of k-step 1 issued
-    // between its MFMAs.
+    // passed the barrier that ended its reads.  Each k-step runs with the
+    // fragments of the next k-step read between its MFMAs; the first also
+    // issues the loads of step kt+NS-1.
     const uint8_t* st = smem[kt % NS];
     issue(kt + NS - 1);
-    read_frags(st, 1, fx[1], fw[1]);
-    mfma_step(fx[0], fw[0]);
 #pragma unroll
-    for (int g = 0; g < NR; ++g) {
-      if (g < LPS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                // LDS read
-      if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+    for (int kk = 0; kk < KS - 1; ++kk) {
+      read_frags(st, kk + 1, fx[(kk + 1) & 1], fw[(kk + 1) & 1]);
+      mfma_step(fx[kk & 1], fw[kk & 1]);
+#pragma unroll
+      for (int g = 0; g < NR; ++g) {
+        if (kk == 0 && g < LPS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                          // LDS read
+        if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
+      }
+      if (kk == 0 && LPS > NR) __builtin_amdgcn_sched_group_barrier(0x020, LPS - NR, 0);
+      if (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
     }
-    if (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
-    // step kt+1 must have landed; the loads of steps kt+2, kt+3 stay in flight
+    // step kt+1 must have landed; the loads of later steps stay in flight
     stage_barrier<LPS>(NS - 2);
-    // k-step 1, with the first fragments of step kt+1 read meanwhile (after
-    // the last step this reads a stage nobody uses)
-    read_frags(smem[(kt + 1) % NS], 0, fx[0], fw[0]);
-    mfma_step(fx[1], fw[1]);
+    // the last k-step, with the first fragments of step kt+1 read meanwhile
+    // (after the last step this reads a stage nobody uses)
+    read_frags(smem[(kt + 1) % NS], 0, fx[KS & 1], fw[KS & 1]);
+    mfma_step(fx[(KS - 1) & 1], fw[(KS - 1) & 1]);
 #pragma unroll
     for (int g = 0; g < NR; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
