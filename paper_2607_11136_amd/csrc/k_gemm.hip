@@ -5,10 +5,11 @@
 // of 64.  Eight waves (two per SIMD) in a 2 x 4 grid each own a (BM/2) x 64
 // sub-tile held as (BM/64) x 2 accumulators of v_mfma_f32_32x32x16.  Operand
 // tiles go from HBM straight into LDS with buffer_load ... lds (no VGPR
-// staging) through two stages: the loads of step k+1 are issued as step k
-// starts and have three of its four MFMA k-steps to land.  Wide steps halve
-// the barriers and give 128-byte row segments (whole cache lines) per load,
-// which measured faster than a four-deep ring of 32-wide steps.  The buffer
+// staging) through two stages.  A step's loads are spread over the two
+// k-steps after the barrier that frees its stage and land by the next
+// barrier.  Wide steps halve the barriers and give 128-byte row segments
+// (whole cache lines) per load, which measured faster than a four-deep ring
+// of 32-wide steps.  The buffer
 // descriptor of each tile covers only that tile's rows, so rows past M read
 // as zero.
 //
@@ -106,25 +107,17 @@ __device__ __forceinline__ void load4f<uint16_t>(const uint16_t* p, float v[4]) 
   v[3] = __uint_as_float(u[1] & 0xffff0000u);
 }
 
-// Workgroup barrier that lets the newest `stages_after` stages of this wave's
-// LDS-bound loads stay in flight: wait for all but the last
-// stages_after * LOADS_PER_STAGE vector-memory loads and for every LDS access,
-// then s_barrier.  (A __syncthreads() would wait for every load.)  The
-// empty asm statements keep the compiler from moving LDS accesses across.
+// Workgroup barrier of the main loop: wait for every LDS-bound load and LDS
+// access of this wave, then s_barrier.  The empty asm statements keep the
+// compiler from moving LDS accesses across; the scheduling fences keep the
+// MFMAs of each k-step on their side of the barrier.
 // s_waitcnt immediate: vmcnt[3:0] in bits 3:0 and vmcnt[5:4] in bits 15:14,
 // expcnt in bits 6:4 (7 = no wait), lgkmcnt in bits 11:8 (0 = wait for all).
-// The scheduling fences keep the MFMAs of each half-step on their side of the
-// barrier, so a wave reaches it with its MFMA queue already full.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
-template <int LOADS_PER_STAGE>
-__device__ __forceinline__ void stage_barrier(int stages_after) {
-  static_assert(2 * LOADS_PER_STAGE < 64, "vmcnt range");
-  static_assert(NS >= 2 && NS <= 4, "at most two stages in flight after the next");
+__device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_sched_barrier(0);
-  if (stages_after >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS_PER_STAGE));
-  else if (stages_after == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS_PER_STAGE));
-  else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
@@ -147,6 +140,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
   constexpr int A_LOADS = BM / NWAVES / RPL, B_LOADS = BN / NWAVES / RPL;  // 1 KiB loads per wave per stage
   static_assert(A_LOADS * NWAVES * RPL == BM && B_LOADS * NWAVES * RPL == BN, "load split");
+  static_assert(NS == 2 && KS >= 2, "two stages of at least two k-steps");
   constexpr int LPS = A_LOADS + B_LOADS;
   typedef typename Mfma<T>::frag frag;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][STAGE_BYTES];
@@ -170,7 +164,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   const int64_t m0 = m_begin + (int64_t)tm * BM;
   const int n0 = tn * BN;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / (BN / WN), wn = wave % (BN / WN);
 
   const T* A = reinterpret_cast<const T*>(p.a);
@@ -203,18 +197,16 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   // (The out-of-range bit is ORed in arithmetically: a select here is turned
   // into branches around each load, which keeps the loads out of the MFMA
   // block.  Tile offsets stay below 2^31, checked by the host.)
-  auto issue = [&](int kt) {
+  auto issue = [&](int kt, int idx) {  // load idx of step kt (A loads, then B loads)
     uint8_t* st = smem[kt % NS];
     const uint32_t oob = (uint32_t)((KT - 1 - kt) >> 31) << 31;  // 0x80000000 once kt >= KT
     const uint32_t kbyte = (uint32_t)(kt * BK * 2);
-#pragma unroll
-    for (int c = 0; c < A_LOADS; ++c) {
-      const uint32_t off = (a_off[c] + kbyte) | oob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * A_LOADS + c) * 1024), 16,
+    if (idx < A_LOADS) {
+      const uint32_t off = (a_off[idx] + kbyte) | oob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * A_LOADS + idx) * 1024), 16,
                                                off, 0, 0, 0);
-    }
-#pragma unroll
-    for (int c = 0; c < B_LOADS; ++c) {
+    } else {
+      const int c = idx - A_LOADS;
       const uint32_t off = (b_off[c] + kbyte) | oob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rb, (lds_ptr_t)(st + A_BYTES + (wave * B_LOADS + c) * 1024), 16, off, 0, 0, 0);
@@ -236,14 +228,12 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   const int b_row0 = (wn * WN + r32) * ROWB;
 
   frag fx[2][MI], fw[2][NJ];
-  auto read_frags = [&](const uint8_t* st, int kk, frag (&x)[MI], frag (&wv)[NJ]) {
+  auto read_one = [&](const uint8_t* st, int kk, int f, frag (&x)[MI], frag (&wv)[NJ]) {
     const int so = (((kk * 2 + hi) ^ sw) * 16);
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-      x[i] = *reinterpret_cast<const frag*>(st + a_row0 + i * 32 * ROWB + so);
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      wv[j] = *reinterpret_cast<const frag*>(st + A_BYTES + b_row0 + j * 32 * ROWB + so);
+    if (f < MI)
+      x[f] = *reinterpret_cast<const frag*>(st + a_row0 + f * 32 * ROWB + so);
+    else
+      wv[f - MI] = *reinterpret_cast<const frag*>(st + A_BYTES + b_row0 + (f - MI) * 32 * ROWB + so);
   };
   auto mfma_step = [&](const frag (&x)[MI], const frag (&wv)[NJ]) {
 #pragma unroll
@@ -253,43 +243,65 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   };
   constexpr int NR = MI + NJ, NM = MI * NJ;  // LDS reads and MFMAs per k-step
 
-  // prologue: steps 0 .. NS-2 in flight; step 0 must land
-  for (int s = 0; s < NS - 1; ++s) issue(s);
-  stage_barrier<LPS>(NS - 2);
-  read_frags(smem[0], 0, fx[0], fw[0]);
+  // Pipeline.  Step kt is consumed from stage kt % 2 over KS k-steps, each
+  // k-step's MFMAs running while the next k-step's fragments are read.  The
+  // barrier before the last k-step of step kt means that every wave has read
+  // all of step kt (its stage is free) and that step kt+1 has landed.  The
+  // loads of step s are issued in two halves: the first during the last
+  // k-step of step s-2, right after the barrier that freed its stage, the
+  // second during the first k-step of step s-1; both land by the barrier of
+  // step s-1.  Spreading them over two k-steps keeps the load address queue
+  // from filling and stalling the MFMA stream.
+  constexpr int H1 = LPS / 2;
+#pragma unroll
+  for (int l = 0; l < LPS; ++l) issue(0, l);
+  stage_barrier();
+#pragma unroll
+  for (int f = 0; f < NR; ++f) read_one(smem[0], 0, f, fx[0], fw[0]);
+#pragma unroll
+  for (int l = 0; l < H1; ++l) issue(1, l);
   for (int kt = 0; kt < KT; ++kt) {
-    // The stage refilled here was consumed at step kt-1, and every wave has
-    // passed the barrier that ended its reads.  Each k-step runs with the
-    // fragments of the next k-step read between its MFMAs; the first also
-    // issues the loads of step kt+NS-1.
     const uint8_t* st = smem[kt % NS];
-    issue(kt + NS - 1);
 #pragma unroll
     for (int kk = 0; kk < KS - 1; ++kk) {
-      read_frags(st, kk + 1, fx[(kk + 1) & 1], fw[(kk + 1) & 1]);
-      mfma_step(fx[kk & 1], fw[kk & 1]);
+      const int nl = kk == 0 ? LPS - H1 : 0;
+      const int ne = NR > nl ? NR : nl;
 #pragma unroll
-      for (int g = 0; g < NR; ++g) {
-        if (kk == 0 && g < LPS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                          // LDS read
-        if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
+      for (int e = 0; e < ne; ++e) {
+        if (e < NR) read_one(st, kk + 1, e, fx[(kk + 1) & 1], fw[(kk + 1) & 1]);
+        if (e < nl) issue(kt + 1, H1 + e);
       }
-      if (kk == 0 && LPS > NR) __builtin_amdgcn_sched_group_barrier(0x020, LPS - NR, 0);
-      if (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
-    }
-    // step kt+1 must have landed; the loads of later steps stay in flight
-    stage_barrier<LPS>(NS - 2);
-    // the last k-step, with the first fragments of step kt+1 read meanwhile
-    // (after the last step this reads a stage nobody uses)
-    read_frags(smem[(kt + 1) % NS], 0, fx[KS & 1], fw[KS & 1]);
-    mfma_step(fx[(KS - 1) & 1], fw[(KS - 1) & 1]);
+      mfma_step(fx[kk & 1], fw[kk & 1]);
+      const int ng = NM > ne ? NM : ne;
 #pragma unroll
-    for (int g = 0; g < NR; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-      if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      for (int g = 0; g < ng; ++g) {
+        if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (g < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        if (g < nl) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
+      }
     }
-    if (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+    stage_barrier();
+    // the last k-step, with the first fragments of step kt+1 read and the
+    // first half of step kt+2 issued into the stage just freed (after the
+    // last step these read a stage nobody uses and load nothing)
+    const int ne = NR > H1 ? NR : H1;
+#pragma unroll
+    for (int e = 0; e < ne; ++e) {
+      if (e < NR) read_one(smem[(kt + 1) % NS], 0, e, fx[KS & 1], fw[KS & 1]);
+      if (e < H1) issue(kt + 2, e);
+    }
+    mfma_step(fx[(KS - 1) & 1], fw[(KS - 1) & 1]);
+    const int ng = NM > ne ? NM : ne;
+#pragma unroll
+    for (int g = 0; g < ng; ++g) {
+      if (g < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      if (g < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      if (g < H1) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
+    }
   }
+  // the out-of-range loads of the last iterations still write zeros to LDS:
+  // let them finish before the workgroup can end
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 
   // Epilogue.  acc[i][j][r] = C[m][n] with m = m0 + wm*(BM/2) + i*32 + r32 and
   // n = n0 + wn*64 + j*32 + 8*(r/4) + 4*hi + r%4.  Every input of a row group
