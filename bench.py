@@ -34,7 +34,7 @@ def attention_flops(B, H, L, d, q_count=None):
 
 # default activation budget per workload (arena bytes)
 DEFAULT_BUDGET = {"tiny": 1 << 30, "image": 2 << 30, "image_b4": 2 << 30, "video": 2 << 30,
-                  "highres": 32 * 10**9, "long": 8 << 30}
+                  "highres": 32 * 10**9, "long": 8 << 30, "video_dual": 2 << 30}
 
 
 def bench_gpu(args, shape):
@@ -55,7 +55,8 @@ def bench_gpu(args, shape):
     w = {k: up(v) for k, v in inp.weights.items()}
     weights = X.block_weights(w)
     cfg = X.block_cfg(shape.hidden, shape.heads, shape.head_dim, shape.mlp_hidden, shape.cond_dim,
-                      shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps)
+                      shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps,
+                      shape.modulation_streams)
     req = X.request(shape.batch, shape.text_len, *shape.grid)
     if args.chunk is not None:
         group = args.batch_group or shape.batch
@@ -142,7 +143,8 @@ def bench_step(args, shape):
     torch.cuda.set_device(0)
     n = args.step_blocks
     cfg = X.block_cfg(shape.hidden, shape.heads, shape.head_dim, shape.mlp_hidden, shape.cond_dim,
-                      shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps)
+                      shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps,
+                      shape.modulation_streams)
     req = X.request(shape.batch, shape.text_len, *shape.grid)
     if args.weight_budget is not None:
         plan = X.xema_offload_plan_budget(cfg, n, args.weight_budget, args.staging)
@@ -308,6 +310,8 @@ WORKLOAD_TEXT = {
                "48x64 heads, MLP 12288, batch 1",
     "long": "long video DiT block: 1024 text + 33x22x38 visual tokens (L=28612), D=4096, 32x128 heads, "
             "MLP 16384, batch 2",
+    "video_dual": "video DiT block 480x720x49f with dual-stream modulation (text tokens' own AdaLN map): "
+                  "226 text + 13x30x45 visual tokens (L=17776), D=3072, 48x64 heads, MLP 12288, batch 1",
 }
 
 
@@ -316,7 +320,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="video", help="tiny, image, image_b4, video, highres or long")
+    ap.add_argument("--workload", default="video", help="tiny, image, image_b4, video, highres, long or video_dual")
     ap.add_argument("--budget", type=int, default=None,
                     help="activation budget (arena bytes); default per workload, 2 GiB for video")
     ap.add_argument("--chunk", type=int, default=None, help="chunk_tokens instead of the planned one")
@@ -339,8 +343,8 @@ def main():
         print(attention_source_digest())
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the block forward is measured on a single MI355X "
-              "(multi-GPU sharding is a design note, not part of this build)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the block forward is measured on a single MI355X; "
+              "sharding it across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
 
     import workloads as W

@@ -57,11 +57,17 @@ typedef enum {
  *   rope_dims   (d_t, d_h, d_w): even widths of the contiguous [t | y | w]
  *               RoPE segments of each head vector, sum <= head_dim
  *   rope_theta  RoPE base (10000 in every shipped config)
- *   ln_eps      LayerNorm epsilon; qk_eps  QK-RMSNorm epsilon            */
+ *   ln_eps      LayerNorm epsilon; qk_eps  QK-RMSNorm epsilon
+ *   modulation_streams  1 (or 0): one AdaLN map modulates every token;
+ *               2: dual-stream block, whose text tokens take their shift,
+ *               scale and gate from a second AdaLN map of their own
+ *               (xema_block_weights.ada_txt_w / ada_txt_b), the visual
+ *               tokens from ada_w / ada_b; every other weight is shared   */
 typedef struct {
   int32_t hidden, heads, head_dim, mlp_hidden, cond_dim;
   int32_t rope_dims[3];
   float rope_theta, ln_eps, qk_eps;
+  int32_t modulation_streams;
 } xema_block_cfg;
 
 /* One batched call: `batch` requests of one template (the paper batches only
@@ -80,10 +86,14 @@ typedef struct {
  *   q_gamma [d]      k_gamma [d]    QK-RMSNorm gains shared by all heads
  *   o_w [D, D]       o_b [D]        attention output projection
  *   up_w [F, D]      up_b [F]       MLP up projection (GELU-tanh follows)
- *   down_w [D, F]    down_b [D]     MLP down projection                    */
+ *   down_w [D, F]    down_b [D]     MLP down projection
+ *   ada_txt_w [6D, D_c]  ada_txt_b [6D]  the text tokens' AdaLN map of a
+ *                                   dual-stream block (modulation_streams = 2),
+ *                                   rows ordered as ada_w; ignored otherwise */
 typedef struct {
   const void *ada_w, *ada_b, *qkv_w, *qkv_b, *q_gamma, *k_gamma;
   const void *o_w, *o_b, *up_w, *up_b, *down_w, *down_b;
+  const void *ada_txt_w, *ada_txt_b;
 } xema_block_weights;
 
 /* A static arena layout: the tensor-id -> offset table of Sec. 8 ("Static
@@ -105,7 +115,7 @@ typedef struct {
  * phase-B weights; phase B (per query chunk) 5 attention, 6 out-projection +
  * gated residual, 7 LN2, 8 MLP up + GELU, 9 MLP down + gated residual.     */
 enum {
-  XEMA_SLOT_MOD = 0,   /* fp32 [B, 6D]                      life [0, 10) */
+  XEMA_SLOT_MOD = 0,   /* fp32 [S, B, 6D], S modulation streams (visual first) life [0, 10) */
   XEMA_SLOT_ROPE,      /* fp32 cos/sin per axis position     life [0, 4)  */
   XEMA_SLOT_Q,         /* fp16 [B, H, Lp, d]                 life [1, 10) */
   XEMA_SLOT_K,         /* fp16 [B, H, Lp, d]                 life [1, 10) */
@@ -171,6 +181,8 @@ XEMA_API int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* 
  * LayerNorm, QKV projection, QK-RMSNorm, 3D RoPE, joint full self-attention,
  * gated output projection, LayerNorm, GELU-tanh MLP, gated residual):
  *   m = W_ada c + b_ada = (shift1, scale1, gate1, shift2, scale2, gate2)
+ *   (a dual-stream block uses m_txt = W_ada_txt c + b_ada_txt on its text
+ *   tokens, positions below text_len, and m on the visual tokens)
  *   h = LN(x)(1 + scale1) + shift1;  [q|k|v] = h W_qkv^T + b_qkv
  *   q, k <- RoPE(RMSNorm(.) * gamma) per head;  o = softmax(q k^T / sqrt(d)) v
  *   x1 = x + gate1 (o W_o^T + b_o);  h2 = LN(x1)(1 + scale2) + shift2

@@ -37,7 +37,7 @@ extern "C" {
  *   n_offloaded          K, blocks whose weights stay in pinned host memory
  *   n_staging            device staging slots (min(requested, K); 0 if K = 0)
  *   offloaded[i]         1 if block i is offloaded (i < n_blocks)
- *   block_weight_bytes   one block's twelve tensors packed into a staging
+ *   block_weight_bytes   one block's weight tensors packed into a staging
  *                        slot, each tensor at a 256-byte boundary
  *   resident_weight_bytes  (N - K) blocks' tensors, unpacked sum
  *   device_weight_bytes  resident + staging: what counts against the budget */

@@ -15,7 +15,8 @@ Modules
 Readings.  The paper names the DiT block but prints none of its arithmetic, so
 the following conventions are readings (they bind the oracle and the HIP path
 alike):
-  R1  one shared weight set for text and visual tokens (single-stream block)
+  R1  one shared weight set for text and visual tokens (single-stream block);
+      R24 is the dual-stream variant
   R2  m = W_ada c + b_ada (no SiLU), split (shift1, scale1, gate1, shift2,
       scale2, gate2); modulation xhat (1 + scale) + shift; residual x + gate * y
   R3  LayerNorm without affine, biased variance, eps 1e-6
@@ -31,6 +32,9 @@ alike):
   R10 conditioning width D_c = D
   R11 synthetic inputs (see the workloads package)
   R17 Algorithm 1 tie-breaks (see layout)
+  R24 dual-stream modulation: a block may carry a second AdaLN map
+      (ada_txt_w, ada_txt_b) whose split modulates the text tokens (positions
+      below L_t); the visual tokens keep m; every other weight is shared
 
 Parity pins: see tests/test_oracle_pins.py and tests/test_layout_oracle.py.
 The conventions R2, R5, R6, R9-R11 are fixed by no value the paper prints, so

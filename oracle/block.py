@@ -25,6 +25,11 @@ docstring.  In short, for each batch element:
   9. g = GELU_tanh(h2 W_1^T + b_1)
  10. out = x1 + gate2 * (g W_2^T + b_2)
 
+Dual-stream modulation (reading R24): when the weights carry a second AdaLN
+map (ada_txt_w, ada_txt_b), the text tokens (positions below L_t) take their
+shift, scale and gate from m_txt = W_ada_txt c + b_ada_txt, split the same way,
+and the visual tokens from m; every other weight stays shared.
+
 Library primitives used as steps: numpy matmul (for the Linear maps and for
 q k^T and P v), numpy exp/tanh/sqrt.  No blocking beyond splitting the query
 rows of step 6 into row groups so memory stays bounded (each query row's
@@ -43,6 +48,18 @@ def adaln_modulation(cond: np.ndarray, w_ada: np.ndarray, b_ada: np.ndarray) -> 
     """m = W_ada c + b_ada for each batch row: [B, D_c] -> [B, 6D].
     Reading R2: a plain linear map of the conditioning vector (no SiLU)."""
     return cond @ w_ada.T + b_ada
+
+
+def row_modulation(cond: np.ndarray, w: Dict[str, np.ndarray], text_len: int, L: int) -> np.ndarray:
+    """The modulation vector of every token: [B, L, 6D].  One AdaLN map for
+    all tokens (reading R1), or with a second map for the text tokens
+    (reading R24): rows below text_len take m_txt, the rest m."""
+    m = adaln_modulation(cond, w["ada_w"], w["ada_b"])
+    rows = np.repeat(m[:, None, :], L, axis=1)
+    if "ada_txt_w" in w:
+        m_txt = adaln_modulation(cond, w["ada_txt_w"], w["ada_txt_b"])
+        rows[:, :text_len, :] = m_txt[:, None, :]
+    return rows
 
 
 def split_modulation(m: np.ndarray) -> Tuple[np.ndarray, ...]:
@@ -195,7 +212,8 @@ def block_forward(x: np.ndarray, cond: np.ndarray, w: Dict[str, np.ndarray], *,
                   coords: Optional[np.ndarray] = None) -> np.ndarray:
     """One DiT block forward in fp64.
 
-    x [B, L, D], cond [B, D_c], w: the twelve weights (fp64).  Returns
+    x [B, L, D], cond [B, D_c], w: the twelve weights (fp64), plus ada_txt_w
+    and ada_txt_b for dual-stream modulation (reading R24).  Returns
     [B, L, D], or [B, len(rows), D] when `rows` selects output rows (keys and
     values are still formed from every token).  `coords` overrides the token
     grid coordinates (used only by tests that move the grid)."""
@@ -204,8 +222,8 @@ def block_forward(x: np.ndarray, cond: np.ndarray, w: Dict[str, np.ndarray], *,
         coords = token_coords(text_len, grid)
     assert coords.shape[0] == L and heads * head_dim == D
     sel = np.arange(L) if rows is None else np.asarray(rows, dtype=np.int64)
-    m = adaln_modulation(cond, w["ada_w"], w["ada_b"])
-    shift1, scale1, gate1, shift2, scale2, gate2 = split_modulation(m)
+    shift1, scale1, gate1, shift2, scale2, gate2 = split_modulation(
+        row_modulation(cond, w, text_len, L))  # each [B, L, D]
     out = np.empty((B, sel.size, D), dtype=np.float64)
     for b in range(B):
         xb = x[b]
@@ -214,10 +232,10 @@ def block_forward(x: np.ndarray, cond: np.ndarray, w: Dict[str, np.ndarray], *,
         o = np.empty((sel.size, heads, head_dim), dtype=np.float64)
         for j in range(heads):
             o[:, j, :] = attention(q[sel, j, :], k[:, j, :], v[:, j, :])
-        x1 = xb[sel] + gate1[b] * linear(o.reshape(sel.size, D), w["o_w"], w["o_b"])
-        h2 = modulate(layer_norm(x1, ln_eps), shift2[b], scale2[b])
+        x1 = xb[sel] + gate1[b][sel] * linear(o.reshape(sel.size, D), w["o_w"], w["o_b"])
+        h2 = modulate(layer_norm(x1, ln_eps), shift2[b][sel], scale2[b][sel])
         g = gelu_tanh(linear(h2, w["up_w"], w["up_b"]))
-        out[b] = x1 + gate2[b] * linear(g, w["down_w"], w["down_b"])
+        out[b] = x1 + gate2[b][sel] * linear(g, w["down_w"], w["down_b"])
     return out
 
 

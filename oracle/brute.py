@@ -66,11 +66,17 @@ def block_forward(x, cond, w: Dict, *, heads: int, head_dim: int, text_len: int,
     D = heads * head_dim
     out = []
     for b in range(B):
-        m = _matvec(w["ada_w"], w["ada_b"], cond[b])
-        sh1, sc1, g1 = m[0:D], m[D:2 * D], m[2 * D:3 * D]
-        sh2, sc2, g2 = m[3 * D:4 * D], m[4 * D:5 * D], m[5 * D:6 * D]
+        m_vis = _matvec(w["ada_w"], w["ada_b"], cond[b])
+        # reading R24: a second AdaLN map, when given, modulates the text tokens
+        m_txt = _matvec(w["ada_txt_w"], w["ada_txt_b"], cond[b]) if "ada_txt_w" in w else m_vis
+
+        def mod(i, part):
+            m = m_txt if i < text_len else m_vis
+            return m[part * D:(part + 1) * D]
+
         qs, ks, vs = [], [], []
         for i in range(L):
+            sh1, sc1 = mod(i, 0), mod(i, 1)
             xh = _ln(x[b][i], ln_eps)
             h = [xh[c] * (1.0 + sc1[c]) + sh1[c] for c in range(D)]
             qkv = _matvec(w["qkv_w"], w["qkv_b"], h)
@@ -102,6 +108,7 @@ def block_forward(x, cond, w: Dict, *, heads: int, head_dim: int, text_len: int,
                 z = sum(p)
                 for e in range(head_dim):
                     o.append(sum(p[t] * vs[t][j][e] for t in range(L)) / z)
+            g1, sh2, sc2, g2 = mod(i, 2), mod(i, 3), mod(i, 4), mod(i, 5)
             ao = _matvec(w["o_w"], w["o_b"], o)
             x1 = [x[b][i][c] + g1[c] * ao[c] for c in range(D)]
             xh2 = _ln(x1, ln_eps)

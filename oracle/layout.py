@@ -103,7 +103,8 @@ def rope_table_bytes(grid: Sequence[int], rope_dims: Sequence[int]) -> int:
 
 
 def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
-                  grid: Sequence[int], rope_dims: Sequence[int], chunk: int) -> List[Tensor]:
+                  grid: Sequence[int], rope_dims: Sequence[int], chunk: int,
+                  modulation_streams: int = 1) -> List[Tensor]:
     """Slot table of one block call with `chunk` tokens per sequence per chunk.
 
     Steps (folded over the chunk loops): 0 = AdaLN map and RoPE table;
@@ -112,12 +113,13 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
     query chunk) 5 = attention, 6 = out-projection with gated residual, 7 = LN2,
     8 = MLP up + GELU, 9 = MLP down + gated residual.  Per-chunk slots are
     reused by every chunk; Q, K, V hold all tokens, padded to a multiple of
-    SEQ_PAD tokens."""
+    SEQ_PAD tokens.  A dual-stream block (reading R24) keeps both modulation
+    vectors, so its mod slot doubles."""
     B, D, F = batch, hidden, mlp_hidden
     c = seq_len if chunk <= 0 or chunk >= seq_len else chunk
     lp = padded_len(seq_len)
     spec = [
-        ("mod", 24 * B * D, 0, 10),
+        ("mod", 24 * B * D * modulation_streams, 0, 10),
         ("rope", rope_table_bytes(grid, rope_dims), 0, 4),
         ("q", 2 * B * D * lp, 1, 10),
         ("k", 2 * B * D * lp, 1, 10),
@@ -139,7 +141,7 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
 def workspace_bytes(shape, chunk: int) -> int:
     """Arena bytes (Algorithm 1 peak) for a workloads.BlockShape and chunk size."""
     ts = block_tensors(shape.batch, shape.seq_len, shape.hidden, shape.mlp_hidden,
-                       shape.grid, shape.rope_dims, chunk)
+                       shape.grid, shape.rope_dims, chunk, shape.modulation_streams)
     return static_layout(ts)[1]
 
 

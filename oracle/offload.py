@@ -19,12 +19,15 @@ from typing import List, Optional, Sequence
 ALIGN = 256
 
 
-def block_weight_sizes(hidden: int, mlp_hidden: int, cond_dim: int, head_dim: int) -> List[int]:
-    """Bytes of the twelve bf16 weight tensors of one block, in the order
-    ada_w, ada_b, qkv_w, qkv_b, q_gamma, k_gamma, o_w, o_b, up_w, up_b,
-    down_w, down_b."""
+def block_weight_sizes(hidden: int, mlp_hidden: int, cond_dim: int, head_dim: int,
+                       modulation_streams: int = 1) -> List[int]:
+    """Bytes of the bf16 weight tensors of one block, in the order ada_w,
+    ada_b, qkv_w, qkv_b, q_gamma, k_gamma, o_w, o_b, up_w, up_b, down_w,
+    down_b, then for a dual-stream block the text tokens' ada_txt_w, ada_txt_b."""
     D, F, Dc, d = hidden, mlp_hidden, cond_dim, head_dim
     elems = [6 * D * Dc, 6 * D, 3 * D * D, 3 * D, d, d, D * D, D, F * D, F, D * F, D]
+    if modulation_streams == 2:
+        elems += [6 * D * Dc, 6 * D]
     return [2 * e for e in elems]
 
 

@@ -37,6 +37,8 @@ SLOT = {n: i for i, n in enumerate(SLOT_NAMES)}
 
 WEIGHT_FIELDS = ("ada_w", "ada_b", "qkv_w", "qkv_b", "q_gamma", "k_gamma",
                  "o_w", "o_b", "up_w", "up_b", "down_w", "down_b")
+# the text tokens' AdaLN map of a dual-stream block (modulation_streams = 2)
+TEXT_MOD_FIELDS = ("ada_txt_w", "ada_txt_b")
 
 
 class XemaError(RuntimeError):
@@ -49,7 +51,8 @@ class BlockCfg(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("mlp_hidden", ctypes.c_int32), ("cond_dim", ctypes.c_int32),
                 ("rope_dims", ctypes.c_int32 * 3), ("rope_theta", ctypes.c_float),
-                ("ln_eps", ctypes.c_float), ("qk_eps", ctypes.c_float)]
+                ("ln_eps", ctypes.c_float), ("qk_eps", ctypes.c_float),
+                ("modulation_streams", ctypes.c_int32)]
 
 
 class Request(ctypes.Structure):
@@ -62,7 +65,7 @@ class Request(ctypes.Structure):
 
 
 class BlockWeights(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS + TEXT_MOD_FIELDS]
 
 
 class Plan(ctypes.Structure):
@@ -195,12 +198,13 @@ def _stream(stream) -> Optional[int]:
 
 def block_cfg(hidden: int, heads: int, head_dim: int, mlp_hidden: int, cond_dim: int,
               rope_dims: Sequence[int], rope_theta: float = 10000.0, ln_eps: float = 1e-6,
-              qk_eps: float = 1e-6) -> BlockCfg:
+              qk_eps: float = 1e-6, modulation_streams: int = 1) -> BlockCfg:
     c = BlockCfg()
     c.hidden, c.heads, c.head_dim, c.mlp_hidden, c.cond_dim = hidden, heads, head_dim, mlp_hidden, cond_dim
     for i in range(3):
         c.rope_dims[i] = int(rope_dims[i])
     c.rope_theta, c.ln_eps, c.qk_eps = rope_theta, ln_eps, qk_eps
+    c.modulation_streams = modulation_streams
     return c
 
 
@@ -211,9 +215,14 @@ def request(batch: int, text_len: int, grid_t: int, grid_h: int, grid_w: int) ->
 
 
 def block_weights(tensors: Dict[str, object]) -> BlockWeights:
+    """The weight struct from named tensors: the twelve of WEIGHT_FIELDS, plus
+    the TEXT_MOD_FIELDS of a dual-stream block when present."""
     w = BlockWeights()
     for n in WEIGHT_FIELDS:
         setattr(w, n, _ptr(tensors[n]))
+    for n in TEXT_MOD_FIELDS:
+        if n in tensors:
+            setattr(w, n, _ptr(tensors[n]))
     return w
 
 

@@ -4,7 +4,8 @@
 // xema_dit_block_fwd runs the block in two phases over token chunks, the
 // "only as much as needed" chunking of Sec. 5.1 applied around DiT attention
 // (Sec. 5.2, "Localized chunking and fusion"):
-//   step 0   AdaLN map (a0) and the RoPE table, once per call
+//   step 0   AdaLN map (a0; two maps for a dual-stream block) and the RoPE
+//            table, once per call
 //   phase A  for each chunk of c tokens: LN1 (a1) -> QKV GEMM (a2) ->
 //            QK-RMSNorm + RoPE scatter (a3), filling Q, K, V^T for all tokens
 //   step 4   fp16 copies of W_o, W_up, W_down
@@ -76,7 +77,8 @@ extern "C" int xema_op_ln_modulate(const void* x, int32_t x_dtype, xema_rowmap x
     return XEMA_ERR_MISALIGNED;
   if (rows == 0) return XEMA_OK;
   return hip_status(launch_ln_modulate(x, x_dtype, to_map(xmap), rows, dim, shift, scale,
-                                       mod_stride, eps, y, y_dtype, (hipStream_t)stream));
+                                       mod_stride, ModSel{0, 0, 0}, eps, y, y_dtype,
+                                       (hipStream_t)stream));
 }
 
 static int check_gemm(const xema_gemm_args* a) {
@@ -117,6 +119,7 @@ static GemmParams to_params(const xema_gemm_args& a) {
   p.c = a.c; p.c_dtype = a.c_dtype; p.c_map = to_map(a.c_map); p.ldc = a.ldc;
   p.resid = a.resid; p.resid_dtype = a.resid_dtype; p.resid_map = to_map(a.resid_map);
   p.ld_resid = a.ld_resid; p.gate = a.gate; p.gate_stride = a.gate_stride;
+  p.gate_sel = ModSel{0, 0, 0};
   return p;
 }
 
@@ -241,9 +244,18 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     if ((expr) != hipSuccess) return XEMA_ERR_HIP; \
   } while (0)
 
+  // A dual-stream block keeps the text tokens' modulation right after the
+  // visual tokens' in the mod slot; rows pick theirs by sequence position.
+  const int64_t txt_delta = dual_stream(c) ? B * 6 * D : 0;
+  auto sel_at = [&](int64_t t0) { return ModSel{t0, r.text_len, txt_delta}; };
+
   // step 0
   XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_w,
                         (const uint16_t*)w.ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s));
+  if (dual_stream(c))
+    XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_txt_w,
+                          (const uint16_t*)w.ada_txt_b, (int)B, (int)Dc, (int)(6 * D),
+                          mod + txt_delta, s));
   XEMA_TRY(launch_rope_table(geom, c.rope_theta, rope, s));
 
   // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk
@@ -251,7 +263,7 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     const int64_t cc = std::min(ch, L - t0);
     const RowMap xmap{cc, L, t0};
     XEMA_TRY(launch_ln_modulate(tokens, x_dtype, xmap, B * cc, (int)D, mod, mod + D, 6 * D,
-                                c.ln_eps, ln1, XEMA_BF16, s));
+                                sel_at(t0), c.ln_eps, ln1, XEMA_BF16, s));
     GemmParams g{};
     g.dtype = XEMA_BF16; g.a = ln1; g.b = w.qkv_w; g.M = B * cc; g.N = (int)(3 * D); g.K = (int)D;
     g.bias = (const uint16_t*)w.qkv_b; g.epilogue = XEMA_EPI_BIAS;
@@ -281,11 +293,11 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     g.bias = (const uint16_t*)w.o_b; g.epilogue = XEMA_EPI_GATED_RESIDUAL;
     g.c = x1; g.c_dtype = XEMA_F32; g.c_map = ident; g.ldc = D;
     g.resid = tokens; g.resid_dtype = x_dtype; g.resid_map = RowMap{cc, L, t0}; g.ld_resid = D;
-    g.gate = mod + 2 * D; g.gate_stride = 6 * D;
+    g.gate = mod + 2 * D; g.gate_stride = 6 * D; g.gate_sel = sel_at(t0);
     XEMA_TRY(launch_gemm(g, s));
 
     XEMA_TRY(launch_ln_modulate(x1, XEMA_F32, ident, B * cc, (int)D, mod + 3 * D, mod + 4 * D,
-                                6 * D, c.ln_eps, ln2, XEMA_F16, s));
+                                6 * D, sel_at(t0), c.ln_eps, ln2, XEMA_F16, s));
 
     GemmParams u{};
     u.dtype = XEMA_F16; u.a = ln2; u.b = wup16; u.M = B * cc; u.N = (int)F; u.K = (int)D;
@@ -298,7 +310,7 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     d.bias = (const uint16_t*)w.down_b; d.epilogue = XEMA_EPI_GATED_RESIDUAL;
     d.c = out; d.c_dtype = XEMA_F32; d.c_map = RowMap{cc, L, t0}; d.ldc = D;
     d.resid = x1; d.resid_dtype = XEMA_F32; d.resid_map = ident; d.ld_resid = D;
-    d.gate = mod + 5 * D; d.gate_stride = 6 * D;
+    d.gate = mod + 5 * D; d.gate_stride = 6 * D; d.gate_sel = sel_at(t0);
     XEMA_TRY(launch_gemm(d, s));
   }
 #undef XEMA_TRY
@@ -317,34 +329,34 @@ static int check_block_call(const xema_block_cfg* cfg, const xema_request* req, 
   if (st != XEMA_OK) return st;
   if (!tokens || !w || !cond || !workspace || !out || workspace_bytes <= 0)
     return XEMA_ERR_INVALID_ARG;
-  const void* wp[12] = {w->ada_w, w->ada_b, w->qkv_w, w->qkv_b, w->q_gamma, w->k_gamma,
-                        w->o_w, w->o_b, w->up_w, w->up_b, w->down_w, w->down_b};
-  for (const void* p : wp)
-    if (!p) return XEMA_ERR_INVALID_ARG;
-  for (const void* p : wp)
-    if (!aligned(p, 16)) return XEMA_ERR_MISALIGNED;
+  const xema_block_cfg& c = *cfg;
+  int64_t wbytes[kWeightTensors];
+  block_weight_sizes(c, wbytes);  // size 0: a tensor the block does not use
+  const void* const* wp = weight_ptrs(*w);
+  for (int i = 0; i < kWeightTensors; ++i)
+    if (wbytes[i] && !wp[i]) return XEMA_ERR_INVALID_ARG;
+  for (int i = 0; i < kWeightTensors; ++i)
+    if (wbytes[i] && !aligned(wp[i], 16)) return XEMA_ERR_MISALIGNED;
   if (!aligned(tokens, 16) || !aligned(cond, 16) || !aligned(out, 16)) return XEMA_ERR_MISALIGNED;
   if (!aligned(workspace, 256)) return XEMA_ERR_MISALIGNED;
 
-  const xema_block_cfg& c = *cfg;
   const xema_request& r = *req;
   const int64_t B = r.batch, L = seq_len(r), D = c.hidden, Dc = c.cond_dim;
   const int64_t out_bytes = B * L * D * 4;
-  int64_t wbytes[12];
-  block_weight_sizes(c, wbytes);
   // out is written while everything else is read: it must overlap nothing
   if (overlaps(out, out_bytes, tokens, B * L * D * 2) ||
       overlaps(out, out_bytes, cond, B * Dc * 2) ||
       overlaps(out, out_bytes, workspace, workspace_bytes))
     return XEMA_ERR_INVALID_ARG;
-  for (int i = 0; i < 12; ++i)
-    if (overlaps(out, out_bytes, wp[i], wbytes[i])) return XEMA_ERR_INVALID_ARG;
+  for (int i = 0; i < kWeightTensors; ++i)
+    if (wbytes[i] && overlaps(out, out_bytes, wp[i], wbytes[i])) return XEMA_ERR_INVALID_ARG;
   // inputs must not live inside the arena the block writes
   if (overlaps(workspace, workspace_bytes, tokens, B * L * D * 2) ||
       overlaps(workspace, workspace_bytes, cond, B * Dc * 2))
     return XEMA_ERR_INVALID_ARG;
-  for (int i = 0; i < 12; ++i)
-    if (overlaps(workspace, workspace_bytes, wp[i], wbytes[i])) return XEMA_ERR_INVALID_ARG;
+  for (int i = 0; i < kWeightTensors; ++i)
+    if (wbytes[i] && overlaps(workspace, workspace_bytes, wp[i], wbytes[i]))
+      return XEMA_ERR_INVALID_ARG;
   return XEMA_OK;
 }
 

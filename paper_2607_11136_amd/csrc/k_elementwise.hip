@@ -66,7 +66,8 @@ __global__ __launch_bounds__(256) void k_adaln(const uint16_t* __restrict__ cond
 
 // ---------------------------------------------------------------------------
 // a1 / a6: LayerNorm + AdaLN modulation.  One wave per row; lane l owns
-// elements [s*256 + 4l, s*256 + 4l + 4) for s = 0 .. dim/256 - 1.
+// elements [s*256 + 4l, s*256 + 4l + 4) for s = 0 .. dim/256 - 1.  A row of
+// a dual-stream block picks its shift/scale by its sequence position (ModSel).
 // ---------------------------------------------------------------------------
 template <typename XT>
 __device__ __forceinline__ void load4(const XT* p, float v[4]);
@@ -98,13 +99,14 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
                                                      int64_t rows, int dim,
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale,
-                                                     int64_t mod_stride, float eps,
+                                                     int64_t mod_stride, ModSel sel, float eps,
                                                      YT* __restrict__ y) {
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
   const int64_t b = r / xmap.rows_per_batch;
-  const int64_t src = b * xmap.batch_stride + xmap.row_offset + (r - b * xmap.rows_per_batch);
+  const int64_t within = r - b * xmap.rows_per_batch;
+  const int64_t src = b * xmap.batch_stride + xmap.row_offset + within;
   const XT* xr = x + src * dim;
   float v[NS][4];
   float s = 0.f;
@@ -125,8 +127,9 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
   }
   const float var = wave_sum(q) / (float)dim;
   const float rstd = 1.0f / sqrtf(var + eps);
-  const float* sh = shift + b * mod_stride;
-  const float* sc = scale + b * mod_stride;
+  const int64_t moff = b * mod_stride + (sel.pos_offset + within < sel.text_len ? sel.text_delta : 0);
+  const float* sh = shift + moff;
+  const float* sc = scale + moff;
   YT* yr = y + r * dim;
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
@@ -339,14 +342,14 @@ hipError_t launch_adaln(const uint16_t* cond, const uint16_t* w, const uint16_t*
 
 template <typename XT, typename YT>
 static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, const float* shift,
-                              const float* scale, int64_t mod_stride, float eps, YT* y,
+                              const float* scale, int64_t mod_stride, ModSel sel, float eps, YT* y,
                               hipStream_t s) {
   const dim3 grid((unsigned)((rows + 3) / 4));
   switch (dim / 256) {
 #define XEMA_LN_CASE(NS)                                                                   \
   case NS:                                                                                 \
     hipLaunchKernelGGL((k_ln_modulate<XT, YT, NS>), grid, dim3(256), 0, s, x, m, rows, dim, \
-                       shift, scale, mod_stride, eps, y);                                  \
+                       shift, scale, mod_stride, sel, eps, y);                             \
     break;
     XEMA_LN_CASE(1) XEMA_LN_CASE(2) XEMA_LN_CASE(3) XEMA_LN_CASE(4) XEMA_LN_CASE(5)
     XEMA_LN_CASE(6) XEMA_LN_CASE(7) XEMA_LN_CASE(8) XEMA_LN_CASE(9) XEMA_LN_CASE(10)
@@ -364,15 +367,15 @@ static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, cons
 
 hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows, int dim,
                               const float* shift, const float* scale, int64_t mod_stride,
-                              float eps, void* y, int y_dtype, hipStream_t s) {
+                              ModSel sel, float eps, void* y, int y_dtype, hipStream_t s) {
   if (x_dtype == XEMA_BF16 && y_dtype == XEMA_BF16)
-    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, eps, (bf16*)y, s);
+    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (bf16*)y, s);
   if (x_dtype == XEMA_BF16 && y_dtype == XEMA_F16)
-    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, eps, (f16*)y, s);
+    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (f16*)y, s);
   if (x_dtype == XEMA_F32 && y_dtype == XEMA_BF16)
-    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, eps, (bf16*)y, s);
+    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (bf16*)y, s);
   if (x_dtype == XEMA_F32 && y_dtype == XEMA_F16)
-    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, eps, (f16*)y, s);
+    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (f16*)y, s);
   return hipErrorInvalidValue;
 }
 

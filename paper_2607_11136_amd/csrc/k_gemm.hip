@@ -332,7 +332,8 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
     if (EPI == XEMA_EPI_GATED_RESIDUAL) {
       const int64_t rrow = b * p.resid_map.batch_stride + p.resid_map.row_offset + within;
       const RT* rrow_ptr = resid + rrow * p.ld_resid;
-      const float* grow = gate + b * p.gate_stride;
+      const float* grow = gate + b * p.gate_stride +
+                          (p.gate_sel.pos_offset + within < p.gate_sel.text_len ? p.gate_sel.text_delta : 0);
       float res[NJ][4][4];
       f32x4 g[NJ][4];
 #pragma unroll

@@ -12,6 +12,14 @@ struct RowMap {
   int64_t rows_per_batch, batch_stride, row_offset;
 };
 
+// Which modulation vector a row of a dual-stream block takes: a row whose
+// sequence position (pos_offset + its index within the batch element's rows)
+// is below text_len reads the text tokens' vectors, text_delta floats past the
+// visual ones.  A single-stream block passes text_delta = 0.
+struct ModSel {
+  int64_t pos_offset, text_len, text_delta;
+};
+
 struct RopeGeom {
   int grid[3];  // (G_t, G_h, G_w)
   int dims[3];  // (d_t, d_h, d_w)
@@ -50,6 +58,7 @@ struct GemmParams {
   int64_t ld_resid;
   const float* gate;
   int64_t gate_stride;
+  ModSel gate_sel;  // per-row choice of the gate vector (positions within c_map's rows)
 };
 
 struct AttnParams {
@@ -64,7 +73,7 @@ hipError_t launch_adaln(const uint16_t* cond, const uint16_t* w, const uint16_t*
                         int cond_dim, int out_dim, float* mod, hipStream_t s);
 hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows, int dim,
                               const float* shift, const float* scale, int64_t mod_stride,
-                              float eps, void* y, int y_dtype, hipStream_t s);
+                              ModSel sel, float eps, void* y, int y_dtype, hipStream_t s);
 hipError_t launch_rope_table(RopeGeom g, float theta, float* table, hipStream_t s);
 hipError_t launch_qk_norm_rope(const QkRopeArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_convert_f16(const uint16_t* src, _Float16* dst, int64_t n, hipStream_t s);

@@ -89,6 +89,7 @@ int validate_shapes(const xema_block_cfg* cfg, const xema_request* req) {
   }
   if (rope_sum > c.head_dim) return XEMA_ERR_INVALID_ARG;
   if (!(c.rope_theta > 0.f) || !(c.ln_eps > 0.f) || !(c.qk_eps > 0.f)) return XEMA_ERR_INVALID_ARG;
+  if (c.modulation_streams < 0 || c.modulation_streams > 2) return XEMA_ERR_INVALID_ARG;
   const int64_t L = seq_len(r);
   if (L <= 0) return XEMA_ERR_INVALID_ARG;
   // what the kernels handle
@@ -100,11 +101,14 @@ int validate_shapes(const xema_block_cfg* cfg, const xema_request* req) {
   return XEMA_OK;
 }
 
-void block_weight_sizes(const xema_block_cfg& c, int64_t bytes[12]) {
+void block_weight_sizes(const xema_block_cfg& c, int64_t bytes[kWeightTensors]) {
   const int64_t D = c.hidden, F = c.mlp_hidden, Dc = c.cond_dim, d = c.head_dim;
-  const int64_t b[12] = {6 * D * Dc * 2, 6 * D * 2, 3 * D * D * 2, 3 * D * 2, d * 2, d * 2,
-                         D * D * 2,      D * 2,     F * D * 2,     F * 2,     D * F * 2, D * 2};
-  for (int i = 0; i < 12; ++i) bytes[i] = b[i];
+  const int64_t t = dual_stream(c) ? 1 : 0;
+  const int64_t b[kWeightTensors] = {6 * D * Dc * 2, 6 * D * 2, 3 * D * D * 2, 3 * D * 2,
+                                     d * 2,          d * 2,     D * D * 2,     D * 2,
+                                     F * D * 2,      F * 2,     D * F * 2,     D * 2,
+                                     t * 6 * D * Dc * 2, t * 6 * D * 2};
+  for (int i = 0; i < kWeightTensors; ++i) bytes[i] = b[i];
 }
 
 int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
@@ -113,7 +117,7 @@ int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t
   const int64_t lp = padded_len(seq_len(req));
   struct Spec { int64_t bytes; int begin, end; };
   const Spec spec[XEMA_NUM_SLOTS] = {
-      {24 * B * D, 0, 10},                         // XEMA_SLOT_MOD
+      {24 * B * D * (dual_stream(cfg) ? 2 : 1), 0, 10},  // XEMA_SLOT_MOD
       {rope_table_bytes(cfg, req), 0, 4},          // XEMA_SLOT_ROPE
       {2 * B * D * lp, 1, 10},                     // XEMA_SLOT_Q
       {2 * B * D * lp, 1, 10},                     // XEMA_SLOT_K

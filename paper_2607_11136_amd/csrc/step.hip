@@ -22,12 +22,13 @@ bool overlaps(const void* a, int64_t an, const void* b, int64_t bn) {
   return a0 < b0 + (uintptr_t)bn && b0 < a0 + (uintptr_t)an;
 }
 
-// Offsets of the twelve tensors packed in a staging slot; returns the slot size.
-int64_t packed_offsets(const xema_block_cfg& c, int64_t off[12]) {
-  int64_t b[12];
+// Offsets of the block's tensors packed in a staging slot (a tensor the block
+// does not use takes no space); returns the slot size.
+int64_t packed_offsets(const xema_block_cfg& c, int64_t off[kWeightTensors]) {
+  int64_t b[kWeightTensors];
   block_weight_sizes(c, b);
   int64_t pos = 0;
-  for (int i = 0; i < 12; ++i) {
+  for (int i = 0; i < kWeightTensors; ++i) {
     off[i] = pos;
     pos += round_up(b[i], kAlign);
   }
@@ -43,11 +44,11 @@ int validate_cfg(const xema_block_cfg* cfg) {
 
 void fill_plan(const xema_block_cfg& c, int n, int k, int staging, xema_offload_plan* out) {
   std::memset(out, 0, sizeof(*out));
-  int64_t off[12], b[12];
+  int64_t off[kWeightTensors], b[kWeightTensors];
   const int64_t slot = packed_offsets(c, off);
   block_weight_sizes(c, b);
   int64_t sum = 0;
-  for (int i = 0; i < 12; ++i) sum += b[i];
+  for (int i = 0; i < kWeightTensors; ++i) sum += b[i];
   out->n_blocks = n;
   out->n_offloaded = k;
   out->n_staging = k > 0 ? std::min(staging, k) : 0;
@@ -59,17 +60,12 @@ void fill_plan(const xema_block_cfg& c, int n, int k, int staging, xema_offload_
   out->device_weight_bytes = out->resident_weight_bytes + out->staging_bytes;
 }
 
-const void* tensor(const xema_block_weights& w, int i) {
-  const void* p[12] = {w.ada_w, w.ada_b, w.qkv_w, w.qkv_b, w.q_gamma, w.k_gamma,
-                       w.o_w,   w.o_b,   w.up_w,  w.up_b,  w.down_w,  w.down_b};
-  return p[i];
-}
+const void* tensor(const xema_block_weights& w, int i) { return weight_ptrs(w)[i]; }
 
-xema_block_weights packed_weights(uint8_t* slot, const int64_t off[12]) {
+xema_block_weights packed_weights(uint8_t* slot, const int64_t off[kWeightTensors]) {
   xema_block_weights w;
-  const void** p[12] = {&w.ada_w, &w.ada_b, &w.qkv_w, &w.qkv_b, &w.q_gamma, &w.k_gamma,
-                        &w.o_w,   &w.o_b,   &w.up_w,  &w.up_b,  &w.down_w,  &w.down_b};
-  for (int i = 0; i < 12; ++i) *p[i] = slot + off[i];
+  const void** p = weight_ptrs(w);
+  for (int i = 0; i < kWeightTensors; ++i) p[i] = slot + off[i];
   return w;
 }
 
@@ -156,10 +152,11 @@ extern "C" int xema_dit_step_fwd(const xema_block_cfg* cfg, const xema_request* 
   st = check_plan(c, plan);
   if (st != XEMA_OK) return st;
   const int N = plan->n_blocks, K = plan->n_offloaded, S = plan->n_staging;
-  int64_t wb[12];
+  int64_t wb[kWeightTensors];
   block_weight_sizes(c, wb);
   for (int i = 0; i < N; ++i)
-    for (int t = 0; t < 12; ++t) {
+    for (int t = 0; t < kWeightTensors; ++t) {
+      if (!wb[t]) continue;  // a tensor the block does not use
       const void* p = tensor(weights[i], t);
       if (!p) return XEMA_ERR_INVALID_ARG;
       if (!aligned(p, 16)) return XEMA_ERR_MISALIGNED;
@@ -182,9 +179,9 @@ extern "C" int xema_dit_step_fwd(const xema_block_cfg* cfg, const xema_request* 
     return XEMA_ERR_INVALID_ARG;
   for (int i = 0; i < N; ++i) {
     if (plan->offloaded[i]) continue;  // host memory cannot alias device buffers
-    for (int t = 0; t < 12; ++t) {
+    for (int t = 0; t < kWeightTensors; ++t) {
       const void* p = tensor(weights[i], t);
-      if (overlaps(out, out_bytes, p, wb[t]) || overlaps(workspace, workspace_bytes, p, wb[t]))
+      if (wb[t] && overlaps(out, out_bytes, p, wb[t]) || overlaps(workspace, workspace_bytes, p, wb[t]))
         return XEMA_ERR_INVALID_ARG;
     }
   }
@@ -192,7 +189,7 @@ extern "C" int xema_dit_step_fwd(const xema_block_cfg* cfg, const xema_request* 
   uint8_t* ws = (uint8_t*)workspace;
   float* resid = (float*)(ws + resid_off);
   uint8_t* staging = ws + staging_off;
-  int64_t off[12];
+  int64_t off[kWeightTensors];
   const int64_t slot_bytes = packed_offsets(c, off);
   const hipStream_t s = (hipStream_t)stream;
   const hipStream_t cs = (hipStream_t)copy_stream;
@@ -218,8 +215,9 @@ extern "C" int xema_dit_step_fwd(const xema_block_cfg* cfg, const xema_request* 
   auto copy_in = [&](int k, hipStream_t q) {
     uint8_t* slot = staging + (int64_t)(k % S) * slot_bytes;
     const xema_block_weights& w = weights[offloaded[k]];
-    for (int t = 0; t < 12; ++t)
-      if (hipMemcpyAsync(slot + off[t], tensor(w, t), wb[t], hipMemcpyHostToDevice, q) != hipSuccess)
+    for (int t = 0; t < kWeightTensors; ++t)
+      if (wb[t] &&
+          hipMemcpyAsync(slot + off[t], tensor(w, t), wb[t], hipMemcpyHostToDevice, q) != hipSuccess)
         return false;
     return true;
   };

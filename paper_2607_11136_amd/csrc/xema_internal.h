@@ -30,8 +30,15 @@ inline int64_t effective_chunk(int64_t L, int64_t chunk) {
 int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
                      xema_plan* out);
 
-// Bytes of one block's twelve weight tensors (order of xema_block_weights).
-void block_weight_sizes(const xema_block_cfg& cfg, int64_t bytes[12]);
+// A block's weight tensors in the order of xema_block_weights: the twelve
+// shared ones, then the text tokens' AdaLN map of a dual-stream block (size 0
+// for a single-stream block).
+constexpr int kWeightTensors = 14;
+inline bool dual_stream(const xema_block_cfg& c) { return c.modulation_streams == 2; }
+void block_weight_sizes(const xema_block_cfg& cfg, int64_t bytes[kWeightTensors]);
+inline const void* const* weight_ptrs(const xema_block_weights& w) { return &w.ada_w; }
+inline const void** weight_ptrs(xema_block_weights& w) { return &w.ada_w; }
+static_assert(sizeof(xema_block_weights) == kWeightTensors * sizeof(void*), "weight struct layout");
 
 }  // namespace xema
 

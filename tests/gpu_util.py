@@ -26,7 +26,7 @@ def f64_to_f16_dev(a: np.ndarray) -> torch.Tensor:
 
 def cfg_of(s: W.BlockShape) -> X.BlockCfg:
     return X.block_cfg(s.hidden, s.heads, s.head_dim, s.mlp_hidden, s.cond_dim, s.rope_dims,
-                       s.rope_theta, s.ln_eps, s.qk_eps)
+                       s.rope_theta, s.ln_eps, s.qk_eps, s.modulation_streams)
 
 
 def req_of(s: W.BlockShape) -> X.Request:

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _cfg(s: W.BlockShape):
     return X.block_cfg(s.hidden, s.heads, s.head_dim, s.mlp_hidden, s.cond_dim, s.rope_dims,
-                       s.rope_theta, s.ln_eps, s.qk_eps)
+                       s.rope_theta, s.ln_eps, s.qk_eps, s.modulation_streams)
 
 
 def _req(s: W.BlockShape):
@@ -51,7 +51,8 @@ def test_layout_matches_oracle(name):
     s = W.CONFIGS[name]
     for chunk in sorted({0, 1, 64, 100, 256, 2048, 8192} | set(s.chunks)):
         p = X.xema_workspace_layout(_cfg(s), _req(s), chunk)
-        ts = OL.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, chunk)
+        ts = OL.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, chunk,
+                              s.modulation_streams)
         offs, peak = OL.static_layout(ts)
         assert p.n_slots == len(ts) == len(X.SLOT_NAMES)
         assert p.workspace_bytes == peak
@@ -203,6 +204,28 @@ def test_fwd_aliasing_rejected():
     assert _fake_call(W.TINY, out_addr=BASE + (1 << 34) + 4096) == X.XEMA_ERR_INVALID_ARG
     assert _fake_call(W.TINY, w_over={"o_w": BASE + (3 << 34) + 1024}) == X.XEMA_ERR_INVALID_ARG
     assert _fake_call(W.TINY, w_over={"down_b": None}) == X.XEMA_ERR_INVALID_ARG
+
+
+def test_dual_stream_validation():
+    s = W.TINY.with_(modulation_streams=2)
+    txt = {"ada_txt_w": BASE + (6 << 34), "ada_txt_b": BASE + (6 << 34) + (1 << 30)}
+    # a dual-stream block needs the text tokens' map (a single-stream one ignores it)
+    assert _fake_call(s) == X.XEMA_ERR_INVALID_ARG
+    assert _fake_call(s, w_over=dict(txt, ada_txt_b=None)) == X.XEMA_ERR_INVALID_ARG
+    assert _fake_call(s, w_over=dict(txt, ada_txt_w=BASE + (6 << 34) + 8)) == X.XEMA_ERR_MISALIGNED
+    assert _fake_call(s, w_over=dict(txt, ada_txt_w=BASE + (2 << 34))) == X.XEMA_ERR_INVALID_ARG  # in out
+    assert _fake_call(s, w_over=dict(txt, ada_txt_b=BASE + (3 << 34) + 512)) == X.XEMA_ERR_INVALID_ARG  # in ws
+    assert _fake_call(s, w_over=txt, ws_bytes=X.xema_workspace_bytes(_cfg(W.TINY), _req(W.TINY), 0)) == \
+        X.XEMA_ERR_WORKSPACE_TOO_SMALL  # the mod slot doubles
+    for streams, ok in ((0, True), (1, True), (2, True), (3, False), (-1, False)):
+        c = _cfg(W.TINY)
+        c.modulation_streams = streams
+        if ok:
+            X.xema_workspace_layout(c, _req(W.TINY), 0)
+        else:
+            with pytest.raises(X.XemaError) as e:
+                X.xema_workspace_layout(c, _req(W.TINY), 0)
+            assert e.value.status == X.XEMA_ERR_INVALID_ARG
 
 
 def test_op_validation():

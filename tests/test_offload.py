@@ -14,11 +14,11 @@ from oracle import step as OS
 
 def _cfg(s):
     return X.block_cfg(s.hidden, s.heads, s.head_dim, s.mlp_hidden, s.cond_dim, s.rope_dims,
-                       s.rope_theta, s.ln_eps, s.qk_eps)
+                       s.rope_theta, s.ln_eps, s.qk_eps, s.modulation_streams)
 
 
 def _sizes(s):
-    return OF.block_weight_sizes(s.hidden, s.mlp_hidden, s.cond_dim, s.head_dim)
+    return OF.block_weight_sizes(s.hidden, s.mlp_hidden, s.cond_dim, s.head_dim, s.modulation_streams)
 
 
 # -- the oracle plan ----------------------------------------------------------------------
@@ -115,7 +115,7 @@ def _same(p, ref, n):
         assert getattr(p, f) == ref[f], f
 
 
-@pytest.mark.parametrize("name", ["tiny", "image", "video", "long"])
+@pytest.mark.parametrize("name", ["tiny", "image", "video", "long", "video_dual"])
 def test_cpp_plan_matches_oracle(name):
     s = W.CONFIGS[name]
     cfg, sizes = _cfg(s), _sizes(s)

@@ -379,3 +379,85 @@ def test_planted_mistakes_are_caught(name, monkeypatch):
     monkeypatch.setattr(O, attr, fn)
     bad = O.block_forward(x, c, w, **_kw(s))
     assert np.max(np.abs(bad - ref)) / np.max(np.abs(ref)) > 1e-9, f"mistake {name} not caught"
+
+
+# -- P13: dual-stream modulation (reading R24) ---------------------------------------------------
+
+
+def _dual(**over):
+    s = W.tiny_shape(modulation_streams=2, **over)
+    return (s,) + _weights(s)
+
+
+def _single(w):
+    return {k: v for k, v in w.items() if k not in W.TEXT_MOD_NAMES}
+
+
+@pytest.mark.parametrize("over", [{}, {"batch": 2}, {"text_len": 1}])
+def test_p13_dual_brute_force_matches(over):
+    s, x, c, w = _dual(**over)
+    a = O.block_forward(x, c, w, **_kw(s))
+    b = _brute(x, c, w, s)
+    rel = np.max(np.abs(a - b)) / np.max(np.abs(b))
+    assert rel <= 1e-12, rel
+    # and the text map does matter
+    assert np.max(np.abs(a - O.block_forward(x, c, _single(w), **_kw(s)))) > 1e-3
+
+
+def test_p13_equal_maps_equal_single_stream():
+    s, x, c, w = _dual()
+    same = dict(w, ada_txt_w=w["ada_w"], ada_txt_b=w["ada_b"])
+    assert np.array_equal(O.block_forward(x, c, same, **_kw(s)),
+                          O.block_forward(x, c, _single(w), **_kw(s)))
+
+
+def test_p13_no_text_tokens_ignores_the_text_map():
+    s, x, c, w = _dual(text_len=0, grid=(2, 3, 2), rope_dims=(4, 4, 2))
+    assert np.array_equal(O.block_forward(x, c, w, **_kw(s)),
+                          O.block_forward(x, c, _single(w), **_kw(s)))
+
+
+@pytest.mark.parametrize("stream", ["text", "visual"])
+def test_p13_zero_gates_of_one_stream_pass_its_tokens_through(stream):
+    s, x, c, w = _dual()
+    D, T = s.hidden, s.text_len
+    w = dict(w)
+    wk, bk = ("ada_txt_w", "ada_txt_b") if stream == "text" else ("ada_w", "ada_b")
+    w[wk], w[bk] = w[wk].copy(), w[bk].copy()
+    for blk in (2, 5):
+        w[wk][blk * D:(blk + 1) * D] = 0.0
+        w[bk][blk * D:(blk + 1) * D] = 0.0
+    out = O.block_forward(x, c, w, **_kw(s))
+    same, moved = (slice(0, T), slice(T, None)) if stream == "text" else (slice(T, None), slice(0, T))
+    assert np.array_equal(out[:, same], x[:, same])
+    assert np.min(np.max(np.abs(out[:, moved] - x[:, moved]), axis=-1)) > 1e-3
+
+
+def _mut_rows_swapped(cond, w, text_len, L):
+    m = O.adaln_modulation(cond, w["ada_w"], w["ada_b"])
+    t = O.adaln_modulation(cond, w["ada_txt_w"], w["ada_txt_b"])
+    rows = np.repeat(t[:, None, :], L, axis=1)
+    rows[:, :text_len, :] = m[:, None, :]
+    return rows
+
+
+def _mut_rows_boundary(cond, w, text_len, L):
+    m = O.adaln_modulation(cond, w["ada_w"], w["ada_b"])
+    t = O.adaln_modulation(cond, w["ada_txt_w"], w["ada_txt_b"])
+    rows = np.repeat(m[:, None, :], L, axis=1)
+    rows[:, :text_len + 1, :] = t[:, None, :]
+    return rows
+
+
+def _mut_rows_text_ignored(cond, w, text_len, L):
+    m = O.adaln_modulation(cond, w["ada_w"], w["ada_b"])
+    return np.repeat(m[:, None, :], L, axis=1)
+
+
+@pytest.mark.parametrize("fn", [_mut_rows_swapped, _mut_rows_boundary, _mut_rows_text_ignored])
+def test_planted_dual_stream_mistakes_are_caught(fn, monkeypatch):
+    s, x, c, w = _dual()
+    ref = _brute(x, c, w, s)
+    monkeypatch.setattr(O, "row_modulation", fn)
+    bad = O.block_forward(x, c, w, **_kw(s))
+    assert np.max(np.abs(bad - ref)) / np.max(np.abs(ref)) > 1e-9

@@ -32,6 +32,8 @@ WEIGHT_NAMES: Tuple[str, ...] = (
     "ada_w", "ada_b", "qkv_w", "qkv_b", "q_gamma", "k_gamma",
     "o_w", "o_b", "up_w", "up_b", "down_w", "down_b",
 )
+# The text tokens' own AdaLN map of a dual-stream block (tensor ids 14, 15).
+TEXT_MOD_NAMES: Tuple[str, ...] = ("ada_txt_w", "ada_txt_b")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -52,6 +54,7 @@ class BlockShape:
     ln_eps: float = 1e-6
     qk_eps: float = 1e-6
     chunks: Tuple[int, ...] = (0,)      # chunk_tokens values exercised; 0 = all
+    modulation_streams: int = 1         # 2: text tokens have their own AdaLN map
 
     @property
     def n_visual(self) -> int:
@@ -74,19 +77,20 @@ class BlockShape:
             "o_w": (D, D), "o_b": (D,),
             "up_w": (F, D), "up_b": (F,),
             "down_w": (D, F), "down_b": (D,),
+            **({"ada_txt_w": (6 * D, Dc), "ada_txt_b": (6 * D,)} if self.modulation_streams == 2 else {}),
         }
 
     def fan_in(self, name: str) -> Optional[int]:
         D, F, Dc = self.hidden, self.mlp_hidden, self.cond_dim
-        return {"ada_w": Dc, "ada_b": Dc, "qkv_w": D, "qkv_b": D,
+        return {"ada_w": Dc, "ada_b": Dc, "ada_txt_w": Dc, "ada_txt_b": Dc, "qkv_w": D, "qkv_b": D,
                 "o_w": D, "o_b": D, "up_w": D, "up_b": D,
                 "down_w": F, "down_b": F}.get(name)
 
     def flops(self) -> int:
         """Algorithmic FLOPs of one block step: the five contractions plus the
-        AdaLN map (elementwise work is not counted)."""
+        AdaLN map(s) (elementwise work is not counted)."""
         B, L, D, F, Dc = self.batch, self.seq_len, self.hidden, self.mlp_hidden, self.cond_dim
-        return (2 * B * Dc * 6 * D + 6 * B * L * D * D + 2 * B * L * D * D
+        return (2 * B * Dc * 6 * D * self.modulation_streams + 6 * B * L * D * D + 2 * B * L * D * D
                 + 4 * B * L * D * F + 4 * B * L * L * D)
 
 
@@ -99,8 +103,12 @@ VIDEO = BlockShape("video", 2, 1, 226, (13, 30, 45), 3072, 48, 64, 12288, 3072, 
 HIGHRES = BlockShape("highres", 3, 1, 226, (13, 68, 120), 3072, 48, 64, 12288, 3072, (16, 24, 24))
 LONG = BlockShape("long", 4, 2, 1024, (33, 22, 38), 4096, 32, 128, 16384, 4096, (32, 48, 48),
                   chunks=(0, 8192, 2048))
+# The video block with dual-stream modulation: the same tensors as VIDEO plus
+# the text tokens' AdaLN map.
+VIDEO_DUAL = VIDEO.with_(name="video_dual", modulation_streams=2)
 
-CONFIGS: Dict[str, BlockShape] = {c.name: c for c in (TINY, IMAGE, IMAGE_B4, VIDEO, HIGHRES, LONG)}
+CONFIGS: Dict[str, BlockShape] = {c.name: c for c in (TINY, IMAGE, IMAGE_B4, VIDEO, HIGHRES, LONG,
+                                                      VIDEO_DUAL)}
 
 
 def _rng(cfg_id: int, tensor_id: int) -> np.random.Generator:
@@ -135,7 +143,7 @@ class Inputs:
     shape: BlockShape
     x: np.ndarray                       # [B, L, D]
     cond: np.ndarray                    # [B, D_c]
-    weights: Dict[str, np.ndarray]      # WEIGHT_NAMES -> array
+    weights: Dict[str, np.ndarray]      # WEIGHT_NAMES (+ TEXT_MOD_NAMES) -> array
 
     def f64(self, name: str) -> np.ndarray:
         if name == "x":
