@@ -11,6 +11,8 @@ Modules
           (Sec. 5.1, the pi* objective) over the block's slot table
   offload the selective weight-offloading plan of an N-block step (Sec. 5.1)
   step    an N-block step: the blocks applied in sequence (Sec. 2.1)
+  vae     the VAE decoder's upsampling stage (Secs. 2.1, 5.2): nearest 2x
+          upsampling, then a 3x3 convolution (reading R25)
 
 Readings.  The paper names the DiT block but prints none of its arithmetic, so
 the following conventions are readings (they bind the oracle and the HIP path
@@ -32,6 +34,8 @@ alike):
   R10 conditioning width D_c = D
   R11 synthetic inputs (see the workloads package)
   R17 Algorithm 1 tie-breaks (see layout)
+  R25 VAE upsampling stage: nearest-neighbour 2x, then 3x3 convolution with
+      zero padding 1 and bias, NHWC activations, weight [C_out, 3, 3, C_in]
   R24 dual-stream modulation: a block may carry a second AdaLN map
       (ada_txt_w, ada_txt_b) whose split modulates the text tokens (positions
       below L_t); the visual tokens keep m; every other weight is shared

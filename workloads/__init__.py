@@ -196,3 +196,56 @@ def step_weights(shape: BlockShape, n_blocks: int) -> List[Dict[str, np.ndarray]
     for i in range(1, n_blocks):
         out.append(make_inputs(shape, seed_id=1000 + 64 * shape.cfg_id + i).weights)
     return out
+
+
+# -- the VAE decoder's upsampling stage -------------------------------------------------------
+
+
+@dataclasses.dataclass(frozen=True)
+class VaeShape:
+    """A VAE decoder upsampling stage: nearest 2x then a 3x3 convolution,
+    NHWC activations of n frames (the decoder runs frame by frame here)."""
+    name: str
+    cfg_id: int
+    n: int            # frames
+    h: int            # input rows
+    w: int            # input columns
+    ci: int           # input channels
+    co: int           # output channels
+
+    def with_(self, **kw) -> "VaeShape":
+        return dataclasses.replace(self, **kw)
+
+    def flops(self) -> int:
+        """Algorithmic FLOPs of the definition: a 3x3 convolution over the
+        2H x 2W upsampled image."""
+        return 2 * self.n * (2 * self.h) * (2 * self.w) * 9 * self.ci * self.co
+
+
+@dataclasses.dataclass
+class VaeInputs:
+    """bf16 bit patterns: x [n, h, w, ci], weight [co, 3, 3, ci], bias [co]."""
+    shape: VaeShape
+    x: np.ndarray
+    weight: np.ndarray
+    bias: np.ndarray
+
+    def f64(self, name: str) -> np.ndarray:
+        return bf16_bits_to_f64(getattr(self, name))
+
+
+def make_vae_inputs(shape: VaeShape) -> VaeInputs:
+    """x ~ N(0, 1); weight and bias ~ N(0, 1 / (9 ci)), the convolution's fan-in."""
+    s = shape
+    std = float(1.0 / np.sqrt(9 * s.ci))
+    return VaeInputs(s, _draw((s.n, s.h, s.w, s.ci), s.cfg_id, 0, 1.0),
+                     _draw((s.co, 3, 3, s.ci), s.cfg_id, 1, std), _draw((s.co,), s.cfg_id, 2, std))
+
+
+# The last upsampler of a 480x720 video decoder (256 channels, 240x360 ->
+# 480x720), over 8 frames, and of a 1080p decoder (540x960 -> 1080x1920) over
+# 2 frames; a small stage for parity tests.
+VAE_TINY = VaeShape("vae_tiny", 20, 2, 5, 7, 64, 256)
+VAE_VIDEO = VaeShape("vae_video", 21, 8, 240, 360, 256, 256)
+VAE_1080P = VaeShape("vae_1080p", 22, 2, 540, 960, 256, 256)
+VAE_CONFIGS: Dict[str, VaeShape] = {c.name: c for c in (VAE_TINY, VAE_VIDEO, VAE_1080P)}
