@@ -148,6 +148,9 @@ _SIGNATURES = {
     "xema_dit_step_fwd": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
                                          ctypes.POINTER(BlockWeights), ctypes.POINTER(OffloadPlan),
                                          _P, _I32, _P, _I64, _P, _P, _P]),
+    "xema_vae_upconv_weight_bytes": (ctypes.c_int, [_I32, _I32, ctypes.POINTER(_I64)]),
+    "xema_vae_upconv_prepare": (ctypes.c_int, [_P, _I32, _I32, _P, _P]),
+    "xema_vae_upconv": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _I32, _I32, _I32, _P, _P]),
 }
 EXPORTED = tuple(_SIGNATURES)
 
@@ -407,3 +410,23 @@ def xema_dit_step_fwd(cfg: BlockCfg, req: Request, tokens, weights: Sequence[Blo
                                    ctypes.byref(plan), _ptr(cond), chunk_tokens, _ptr(workspace),
                                    int(workspace_bytes), _ptr(out), _stream(stream), cs),
            "xema_dit_step_fwd")
+
+
+# -- the VAE decoder's fused upsampling stage (include/xema_vae.h) -------------------------------
+
+
+def xema_vae_upconv_weight_bytes(ci: int, co: int) -> int:
+    n = _I64()
+    _check(lib().xema_vae_upconv_weight_bytes(ci, co, ctypes.byref(n)), "xema_vae_upconv_weight_bytes")
+    return n.value
+
+
+def xema_vae_upconv_prepare(w, ci: int, co: int, wp, stream=None) -> None:
+    _check(lib().xema_vae_upconv_prepare(_ptr(w), ci, co, _ptr(wp), _stream(stream)),
+           "xema_vae_upconv_prepare")
+
+
+def xema_vae_upconv(x, n: int, h: int, w: int, ci: int, wp, bias, co: int, row_begin: int,
+                    row_count: int, y, stream=None) -> None:
+    _check(lib().xema_vae_upconv(_ptr(x), n, h, w, ci, _ptr(wp), _ptr(bias), co, row_begin, row_count,
+                                 _ptr(y), _stream(stream)), "xema_vae_upconv")

@@ -69,6 +69,19 @@ struct AttnParams {
   int batch, heads, seq_len, padded_len, q_begin, q_count;
 };
 
+// The VAE decoder's fused upsampling stage (k_upconv.hip).
+struct UpconvParams {
+  const uint16_t* x;     // bf16 [n, h, w, ci]
+  const uint16_t* wp;    // bf16 phase-summed weights [4][co][4][ci]
+  const uint16_t* bias;  // bf16 [co]
+  uint16_t* y;           // bf16 [n, 2h, 2w, co]
+  int n, h, w, ci, co;
+  int row_begin, row_count;  // source rows computed; output rows 2*row_begin ..
+};
+
+hipError_t launch_upconv_prep(const uint16_t* w, int ci, int co, uint16_t* wp, hipStream_t s);
+hipError_t launch_upconv(const UpconvParams& p, hipStream_t s);
+
 hipError_t launch_adaln(const uint16_t* cond, const uint16_t* w, const uint16_t* bias, int batch,
                         int cond_dim, int out_dim, float* mod, hipStream_t s);
 hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows, int dim,

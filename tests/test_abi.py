@@ -26,7 +26,7 @@ def _req(s: W.BlockShape):
 
 def _declared_symbols():
     names = set()
-    for h in ("xema.h", "xema_ops.h", "xema_step.h"):
+    for h in ("xema.h", "xema_ops.h", "xema_step.h", "xema_vae.h"):
         src = open(os.path.join(ROOT, "include", h)).read()
         names.update(re.findall(r"XEMA_API\s+[\w\s\*]+?\b(xema_\w+)\s*\(", src))
     return names
@@ -35,7 +35,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = X.lib()
     declared = _declared_symbols()
-    assert len(declared) == 19, declared
+    assert len(declared) == 22, declared
     for name in declared:
         assert hasattr(lib, name), name
     assert declared == set(X.EXPORTED)
@@ -226,6 +226,28 @@ def test_dual_stream_validation():
             with pytest.raises(X.XemaError) as e:
                 X.xema_workspace_layout(c, _req(W.TINY), 0)
             assert e.value.status == X.XEMA_ERR_INVALID_ARG
+
+
+def test_vae_upconv_validation():
+    lib = X.lib()
+    n = ctypes.c_int64()
+    assert lib.xema_vae_upconv_weight_bytes(256, 512, ctypes.byref(n)) == X.XEMA_OK and n.value == 32 * 256 * 512
+    assert lib.xema_vae_upconv_weight_bytes(96, 256, ctypes.byref(n)) == X.XEMA_ERR_UNSUPPORTED
+    assert lib.xema_vae_upconv_weight_bytes(64, 128, ctypes.byref(n)) == X.XEMA_ERR_UNSUPPORTED
+    assert lib.xema_vae_upconv_weight_bytes(0, 256, ctypes.byref(n)) == X.XEMA_ERR_INVALID_ARG
+    x, wp, b, y = BASE, BASE + (1 << 34), BASE + (2 << 34), BASE + (3 << 34)
+    f = lib.xema_vae_upconv
+    # every case fails validation before any launch
+    assert f(None, 1, 4, 4, 64, wp, b, 256, 0, 4, y, None) == X.XEMA_ERR_INVALID_ARG
+    assert f(x, 1, 4, 4, 64, wp, b, 256, 3, 2, y, None) == X.XEMA_ERR_INVALID_ARG      # rows past h
+    assert f(x, 1, 4, 4, 64, wp, b, 256, -1, 2, y, None) == X.XEMA_ERR_INVALID_ARG
+    assert f(x, 1, 4, 4, 64, wp, b, 256, 0, 0, y, None) == X.XEMA_ERR_INVALID_ARG
+    assert f(x, 1, 4, 4, 80, wp, b, 256, 0, 4, y, None) == X.XEMA_ERR_UNSUPPORTED
+    assert f(x, 64, 512, 512, 128, wp, b, 256, 0, 4, y, None) == X.XEMA_ERR_UNSUPPORTED  # input >= 2 GiB
+    assert f(x + 8, 1, 4, 4, 64, wp, b, 256, 0, 4, y, None) == X.XEMA_ERR_MISALIGNED
+    assert f(x, 1, 4, 4, 64, wp, b, 256, 0, 4, x + 256, None) == X.XEMA_ERR_INVALID_ARG  # y overlaps x
+    assert lib.xema_vae_upconv_prepare(wp, 64, 256, wp + 1024, None) == X.XEMA_ERR_INVALID_ARG  # overlap
+    assert lib.xema_vae_upconv_prepare(wp + 4, 64, 256, y, None) == X.XEMA_ERR_MISALIGNED
 
 
 def test_op_validation():
