@@ -235,6 +235,101 @@ def bench_step(args, shape):
     print(json.dumps(result), flush=True)
 
 
+def bench_vae(args):
+    """The VAE decoder's fused upsampling stage (nearest 2x + 3x3 conv) over a
+    whole stage of frames, inputs resident in HBM.  Prints one JSON line."""
+    import torch
+
+    import paper_2607_11136_amd as X
+    import workloads as W
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    s = W.VAE_CONFIGS[args.vae]
+    g = torch.Generator(device=dev).manual_seed(2607)
+    std = 1.0 / (9 * s.ci) ** 0.5
+    x = torch.randn((s.n, s.h, s.w, s.ci), device=dev, generator=g).to(torch.bfloat16)
+    w = (torch.randn((s.co, 3, 3, s.ci), device=dev, generator=g) * std).to(torch.bfloat16)
+    b = (torch.randn((s.co,), device=dev, generator=g) * std).to(torch.bfloat16)
+    wp = torch.empty(X.xema_vae_upconv_weight_bytes(s.ci, s.co) // 2, dtype=torch.bfloat16, device=dev)
+    y = torch.empty((s.n, 2 * s.h, 2 * s.w, s.co), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+    X.xema_vae_upconv_prepare(w, s.ci, s.co, wp, stream)
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+
+    def run():
+        X.xema_vae_upconv(x, s.n, s.h, s.w, s.ci, wp, b, s.co, 0, s.h, y, stream)
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        run()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    fused_peak = int(torch.cuda.max_memory_allocated())
+    context = None
+    if args.vae_torch_context:
+        # the same stage unfused through PyTorch (nearest interpolate, then a
+        # bf16 channels-last Conv2d), for context only
+        xt = x.permute(0, 3, 1, 2)                     # NCHW view of the NHWC tensor
+        wt = w.permute(0, 3, 1, 2).contiguous(memory_format=torch.channels_last)
+        del y
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+
+        def unfused():
+            u = torch.nn.functional.interpolate(xt, scale_factor=2, mode="nearest")
+            return torch.nn.functional.conv2d(u, wt, b, padding=1)
+
+        with torch.no_grad():
+            for _ in range(2):
+                yt = unfused()
+            del yt
+            torch.cuda.synchronize()
+            c0 = torch.cuda.Event(enable_timing=True)
+            c1 = torch.cuda.Event(enable_timing=True)
+            c0.record(stream)
+            for _ in range(3):
+                yt = unfused()
+                del yt
+            c1.record(stream)
+            torch.cuda.synchronize()
+        context = {"torch_unfused_ms": round(c0.elapsed_time(c1) / 3, 3),
+                   "torch_unfused_extra_peak_bytes": int(torch.cuda.max_memory_allocated() - base)}
+    flops = s.flops()                      # the definition: 3x3 over the upsampled image
+    mfma_flops = flops * 16 // 36          # what the phase form executes
+    up_bytes = s.n * 4 * s.h * s.w * s.ci * 2
+    result = {
+        "metric": "VAE upsampling stage ms (nearest 2x + 3x3 conv, fused)",
+        "value": round(ms, 4),
+        "unit": "ms",
+        "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "tflops_definition": round(flops / (ms * 1e-3) / 1e12, 1),
+        "dtype": "bf16",
+        "data": "synthetic (random N(0,1) activations, N(0,1/(9 ci)) weights)",
+        "config": {"workload": f"{s.name}: {s.n} frames {s.h}x{s.w} -> {2 * s.h}x{2 * s.w}, "
+                               f"{s.ci} -> {s.co} channels",
+                   "flops_definition": flops, "mfma_flops": mfma_flops,
+                   "input_bytes": s.n * s.h * s.w * s.ci * 2, "output_bytes": s.n * 4 * s.h * s.w * s.co * 2,
+                   "upsampled_bytes_not_stored": up_bytes,
+                   "device_peak_bytes": fused_peak},
+        "roofline": {"kernel": "k_upconv (four 2x2 phase convolutions, implicit GEMM)", "bound": "mfma",
+                     "achieved": round(mfma_flops / (ms * 1e-3) / 1e12, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": round(mfma_flops / (ms * 1e-3) / 1e12 / 2500.0, 4)},
+    }
+    if context:
+        result["context"] = context
+    print(json.dumps(result), flush=True)
+
+
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attention_video_hbm_traffic.md")
 TRAFFIC_SOURCES = ("paper_2607_11136_amd/csrc/k_attention.hip", "paper_2607_11136_amd/csrc/device_common.h",
                    "paper_2607_11136_amd/csrc/kernels.h")
@@ -334,6 +429,9 @@ def main():
                     help="device weight budget in bytes; the plan picks the smallest K (step mode)")
     ap.add_argument("--staging", type=int, default=2, help="device staging slots (step mode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--vae", default=None, help="time the VAE upsampling stage vae_video or vae_1080p instead")
+    ap.add_argument("--vae-torch-context", action="store_true",
+                    help="with --vae, also time the stage unfused through PyTorch (context only)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="also run a plain device copy of this size (calibrates HBM byte counters)")
     ap.add_argument("--print-digest", action="store_true",
@@ -347,6 +445,9 @@ def main():
               "sharding it across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
 
+    if args.vae:
+        bench_vae(args)
+        return
     import workloads as W
     shape = W.CONFIGS[args.workload]
     if args.step_blocks > 0:
