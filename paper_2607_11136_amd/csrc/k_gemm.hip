@@ -76,6 +76,16 @@ __host__ __device__ constexpr int row_swz(int r) { return (r >> 1) & 7; }
 constexpr int NJ = WN / 32;                // 32-column MFMA blocks per wave
 constexpr int BUF_FLAGS = 0x00020000;      // raw buffer, 32-bit dwords
 
+// 16 bytes per lane from buffer offset voff + soff straight into LDS (one
+// 1 KiB wave row at dst).  The host pass cannot check this builtin with a
+// run-time scalar offset, so it sees an empty body.
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, uint8_t* dst, uint32_t voff,
+                                           uint32_t soff) {
+#if __HIP_DEVICE_COMPILE__
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 16, voff, soff, 0, 0);
+#endif
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                            BUF_FLAGS);
@@ -176,9 +186,10 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   // Direct-to-LDS load plan: a 1 KiB wave instruction fills RPL rows; wave w
   // fills A rows (BM/NWAVES) w .. and B rows (BN/NWAVES) w ..  Lane l writes
   // row l / SLOTS of its chunk at physical slot l % SLOTS, so it fetches the
-  // logical slot that the row's swizzle maps there.  The whole offset is in
-  // the VGPR operand, which is what the buffer range check covers (rows past
-  // M read as zero).
+  // logical slot that the row's swizzle maps there.  The row offset is the
+  // VGPR operand, which the buffer range check covers: a row past M is out of
+  // range whatever the K offset and reads zero, and a row inside stays inside
+  // (row K + slot + k < (row + 1) K elements).
   uint32_t a_off[A_LOADS], b_off[B_LOADS];
 #pragma unroll
   for (int c = 0; c < A_LOADS; ++c) {
@@ -191,25 +202,19 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
     b_off[c] = (uint32_t)((row * K + (((lane % SLOTS) ^ row_swz(row)) * 8)) * 2);
   }
 
-  // A step past the last one is issued at an offset beyond the descriptor's
-  // range: the hardware moves no data (the lanes read as zero) and the loop
-  // body stays free of branches, so its loads can be spread between MFMAs.
-  // (The out-of-range bit is ORed in arithmetically: a select here is turned
-  // into branches around each load, which keeps the loads out of the MFMA
-  // block.  Tile offsets stay below 2^31, checked by the host.)
+  // The per-lane offsets above are loop-invariant: a step's K offset goes in
+  // the instruction's scalar offset, so issuing a load costs no vector ALU
+  // work.  A step past the last one (the pipeline runs two ahead) reloads the
+  // last step into a stage nobody reads, which keeps the loop free of
+  // branches.  Tile offsets stay below 2^31, checked by the host.
   auto issue = [&](int kt, int idx) {  // load idx of step kt (A loads, then B loads)
     uint8_t* st = smem[kt % NS];
-    const uint32_t oob = (uint32_t)((KT - 1 - kt) >> 31) << 31;  // 0x80000000 once kt >= KT
-    const uint32_t kbyte = (uint32_t)(kt * BK * 2);
+    const uint32_t kbyte = (uint32_t)((kt < KT ? kt : KT - 1) * BK * 2);
     if (idx < A_LOADS) {
-      const uint32_t off = (a_off[idx] + kbyte) | oob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * A_LOADS + idx) * 1024), 16,
-                                               off, 0, 0, 0);
+      load_lds16(ra, st + (wave * A_LOADS + idx) * 1024, a_off[idx], kbyte);
     } else {
       const int c = idx - A_LOADS;
-      const uint32_t off = (b_off[c] + kbyte) | oob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rb, (lds_ptr_t)(st + A_BYTES + (wave * B_LOADS + c) * 1024), 16, off, 0, 0, 0);
+      load_lds16(rb, st + A_BYTES + (wave * B_LOADS + c) * 1024, b_off[c], kbyte);
     }
   };
 
@@ -299,8 +304,8 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
       if (g < H1) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global->LDS load
     }
   }
-  // the out-of-range loads of the last iterations still write zeros to LDS:
-  // let them finish before the workgroup can end
+  // the reloads of the last iterations still write to LDS: let them finish
+  // before the workgroup can end
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 
   // Epilogue.  acc[i][j][r] = C[m][n] with m = m0 + wm*(BM/2) + i*32 + r32 and
