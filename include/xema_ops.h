@@ -113,7 +113,9 @@ XEMA_API int xema_op_qk_norm_rope(const xema_block_cfg* cfg, const xema_request*
  * multiple of XEMA_SEQ_PAD with seq_len <= padded_len, and the padding
  * columns of vt must be finite (xema_op_qk_norm_rope zeroes them).  Keys are
  * visited in one fixed ascending order; each query's result depends only on
- * that query and the keys.  head_dim 64 or 128.                              */
+ * that query and the keys.  head_dim 64 or 128.  The exponents qs_i . k_j
+ * must stay below 2^16 in magnitude (the d = 64 kernel keeps its reference
+ * max in fp16); RMS-normalised queries and keys are far inside that.        */
 XEMA_API int xema_op_attention(const void* q, const void* k, const void* vt, int32_t batch,
                       int32_t heads, int32_t head_dim, int32_t seq_len, int32_t padded_len,
                       int32_t q_begin, int32_t q_count, void* o, void* stream);

@@ -25,7 +25,11 @@
 //   k_attention_lazy (used at d = 64): two column blocks per wave (half the
 //     LDS reads per score), a 2-stage ring, and a trigger on the tile max
 //     exceeding the reference by TAU = 8 (v_max3 reductions), which leaves the
-//     exponentials out of the branch; row sums by v_dot2 as above.
+//     exponentials out of the branch; row sums by v_dot2 as above.  The
+//     reference is subtracted by the MFMA: one more k-step multiplies a
+//     column of ones in the key operand by -mrow in the query operand (kept
+//     fp16-representable), which costs 4 MFMAs per tile instead of 64
+//     subtractions per lane.  Scores must stay below 2^16 in log2 units.
 // Measured on the workloads' own Q/K/V, each is the faster one at its width.
 //
 // Keys are visited in one fixed ascending order of 64-key tiles, and every
@@ -145,7 +149,29 @@ struct WaveState {
   f32x16 minit[QB];          // -mrow in all 16 entries
   float mrow[QB];            // reference max in use (log2 units)
   float lrow[QB];            // this lane's share of the row sum
+  f16x8 mneg[QB];            // B fragment of the extra k-step: -mrow at k = 0
 };
+
+// S^T - mrow for two 32-key blocks x QB query columns: the score MFMAs plus
+// one k-step of (a column of ones) x (-mrow), so the scores arrive shifted.
+template <int HD, int QB>
+__device__ __forceinline__ void tile_scores_ones(const uint8_t* Ks, const f16x8 (&qf)[QB][HD / 16],
+                                                 const f16x8 (&mneg)[QB], f16x8 ones, int krow,
+                                                 int kswz, int hi, f32x16 (&s)[2][QB]) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int row = kb * 32 + krow;
+#pragma unroll
+    for (int kk = 0; kk < HD / 16; ++kk) {
+      const int slot16 = (kk * 2 + hi) ^ kswz;
+      const f16x8 kf = *reinterpret_cast<const f16x8*>(Ks + row * (HD * 2) + slot16 * 16);
+#pragma unroll
+      for (int c = 0; c < QB; ++c) s[kb][c] = mma(kf, qf[c][kk], kk == 0 ? f32x16{} : s[kb][c]);
+    }
+#pragma unroll
+    for (int c = 0; c < QB; ++c) s[kb][c] = mma(ones, mneg[c], s[kb][c]);
+  }
+}
 
 // S^T = K Q^T - mrow for two 32-key blocks x QB query columns
 template <int HD, int QB, bool MI>
@@ -230,14 +256,18 @@ __device__ __forceinline__ void tile_softmax(const f32x16 (&s)[2][QB], bool firs
   for (int c = 0; c < QB; ++c) st.lrow[c] += lsp[c];
 }
 
-// Online softmax of one tile for k_attention_lazy: scores arrive unshifted;
-// a column grows when its tile max exceeds mrow by more than TAU (and on the
-// first tile), and only then do mrow move and O and the row sum get rescaled.
-// P = 2^(s - mrow) <= 2^TAU; the row sum is the v_dot2 sum of the packed P.
+// Online softmax of one tile for k_attention_lazy.  The scores arrive as
+// s - mrow (the extra k-step of tile_scores_ones), so the common path takes
+// P = 2^s straight from the MFMA output.  A column grows when its tile max
+// exceeds TAU (and on the first tile): mrow moves to the tile max, rounded to
+// fp16 because it feeds the MFMA, O and the row sum are rescaled, and the
+// tile's scores are shifted in place.  Columns that do not grow shift by 0
+// and scale by 1.0, so a query's result never depends on the others of its
+// wave.  The row sum is the v_dot2 sum of the packed P.
 template <int HD, int QB>
-__device__ __forceinline__ void tile_softmax_maxtrig(const f32x16 (&s)[2][QB], bool first,
-                                                     WaveState<HD, QB>& st,
-                                                     f16x8 (&pf)[QB][2][2]) {
+__device__ __forceinline__ void tile_softmax_ones(f32x16 (&s)[2][QB], bool first,
+                                                  WaveState<HD, QB>& st, f16x8 (&pf)[QB][2][2],
+                                                  int hi) {
   float mxs[QB];
   bool grow_any = first;
 #pragma unroll
@@ -248,25 +278,35 @@ __device__ __forceinline__ void tile_softmax_maxtrig(const f32x16 (&s)[2][QB], b
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][c][r]);
     mxs[c] = pair_max(mx);
-    grow_any |= mxs[c] - st.mrow[c] > TAU;
+    grow_any |= mxs[c] > TAU;
   }
   if (__builtin_amdgcn_ballot_w64(grow_any)) {
 #pragma unroll
     for (int c = 0; c < QB; ++c) {
-      const bool grow = first || mxs[c] - st.mrow[c] > TAU;
-      const float alpha = first ? 0.f : (grow ? fast_exp2(st.mrow[c] - mxs[c]) : 1.f);
-      if (grow) st.mrow[c] = mxs[c];
+      const bool grow = first || mxs[c] > TAU;
+      float shift = 0.f;
+      if (grow) {
+        const float mnew = (float)(f16)(st.mrow[c] + mxs[c]);
+        shift = mnew - st.mrow[c];
+        st.mrow[c] = mnew;
+      }
+      const float alpha = first ? 0.f : (grow ? fast_exp2(-shift) : 1.f);
       st.lrow[c] *= alpha;
 #pragma unroll
       for (int d = 0; d < HD / 32; ++d)
 #pragma unroll
         for (int r = 0; r < 16; ++r) st.oacc[c][d][r] *= alpha;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][c][r] -= shift;   // x - 0 = x for the others
+      f16x8 mn = {};
+      mn[0] = hi ? (f16)0.f : (f16)(-st.mrow[c]);
+      st.mneg[c] = mn;
     }
   }
 #pragma unroll
-  for (int c = 0; c < QB; ++c) {
-    st.lrow[c] += exp_pack<true>(s[0][c], s[1][c], st.mrow[c], pf[c]);
-  }
+  for (int c = 0; c < QB; ++c) st.lrow[c] += exp_pack<false>(s[0][c], s[1][c], 0.f, pf[c]);
 }
 
 // O^T += V^T P^T
@@ -463,9 +503,11 @@ __device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int 
                                             (uint32_t)((kv + 1) * KV * 2));
   f32x16 s[2][QB];
   f16x8 pf[QB][2][2];
-  tile_scores<HD, QB, false>(smem[stage], qf, st.minit, krow, kswz, hi, s);
+  f16x8 ones = {};
+  ones[0] = hi ? (f16)0.f : (f16)1.f;
+  tile_scores_ones<HD, QB>(smem[stage], qf, st.mneg, ones, krow, kswz, hi, s);
   if (LAST && tail < KV) mask_tail<QB>(s, tail, hi);
-  tile_softmax_maxtrig<HD, QB>(s, kv == 0, st, pf);
+  tile_softmax_ones<HD, QB>(s, kv == 0, st, pf, hi);
   tile_pv<HD, QB>(smem[stage] + K_BYTES, pf, r32, hi, st.oacc);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -545,6 +587,7 @@ __global__ __launch_bounds__(NW * 64) void k_attention_lazy(AttnParams p) {
     st.lrow[c] = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) st.minit[c][r] = 0.f;
+    st.mneg[c] = f16x8{};
 #pragma unroll
     for (int d = 0; d < NDB; ++d)
 #pragma unroll
