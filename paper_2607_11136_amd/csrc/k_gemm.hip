@@ -13,11 +13,12 @@
 // descriptor of each tile covers only that tile's rows, so rows past M read
 // as zero.
 //
-// A launch covers a range of rows.  The launcher splits the rows between a
-// 256-row-tile launch and a 128-row-tile launch so that the last wave of
-// workgroups over the 256 CUs is as full as possible (e.g. 17776 x 3072 is
-// 840 tiles of 256 x 256 = 3.3 waves; 64 tile-rows of 256 plus 11 of 128 fill
-// 3 waves and half a wave of half-size tiles).
+// One launch covers the rows in two tile heights: the first rows in 256-row
+// tiles, the rest in 128-row tiles dispatched last, which fill the CUs the
+// last round of full tiles leaves idle.  The launcher picks the split from a
+// model of the completion time (e.g. 17776 x 3072 is 840 tiles of 256 x 256,
+// four rounds over 256 CUs with the last 28% full; 54 tile-rows of 256 and 31
+// of 128 finish in about 3.6 rounds).
 //
 // LDS layout: a stage holds BM rows of A and 256 rows of B, 64 elements (128
 // bytes = eight 16-byte slots) each; slot j of row r is stored at slot
@@ -37,6 +38,9 @@
 // steps, one MFMA each, in the same sequence whatever M, BM, the row maps
 // or the tile position are; so chunked and unchunked calls, and either tile
 // height, agree bit for bit.
+#include <algorithm>
+#include <vector>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -136,14 +140,15 @@ __device__ __forceinline__ void stage_barrier() {
 
 }  // namespace
 
-// EPI: XEMA_EPI_BIAS / XEMA_EPI_BIAS_GELU (CT = bf16 or f16) or
-// XEMA_EPI_GATED_RESIDUAL (CT = float, RT = residual element type).  Rows
-// [m_begin, M) in tiles of BM rows.
+// One BM x 256 output tile.  EPI: XEMA_EPI_BIAS / XEMA_EPI_BIAS_GELU (CT =
+// bf16 or f16) or XEMA_EPI_GATED_RESIDUAL (CT = float, RT = residual element
+// type).  Rows [m_begin, m_end) in tiles of BM rows; wg numbers this tile
+// among them; smem_raw holds the two LDS stages.
 template <typename T, int EPI, typename CT, typename RT, int BM>
-__global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m_begin,
-                                                 const uint16_t* __restrict__ bias,
-                                                 CT* __restrict__ cout, const RT* __restrict__ resid,
-                                                 const float* __restrict__ gate) {
+__device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, int64_t m_end, int wg,
+                                          uint8_t* smem_raw, const uint16_t* __restrict__ bias,
+                                          CT* __restrict__ cout, const RT* __restrict__ resid,
+                                          const float* __restrict__ gate) {
   static_assert(BM == 256 || BM == 128, "tile heights");
   constexpr int MI = BM / 64;                         // 32-row MFMA blocks per wave
   constexpr int A_BYTES = BM * BK * 2;
@@ -153,15 +158,14 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
   static_assert(NS == 2 && KS >= 2, "two stages of at least two k-steps");
   constexpr int LPS = A_LOADS + B_LOADS;
   typedef typename Mfma<T>::frag frag;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS][STAGE_BYTES];
+  uint8_t (*smem)[STAGE_BYTES] = reinterpret_cast<uint8_t (*)[STAGE_BYTES]>(smem_raw);
 
   const int K = p.K;
   const int KT = K / BK;
-  const int tiles_m = (int)((p.M - m_begin + BM - 1) / BM);
+  const int tiles_m = (int)((m_end - m_begin + BM - 1) / BM);
   const int tiles_n = p.N / BN;
   const int total = tiles_m * tiles_n;
   // XCD-aware tile order (see the file comment)
-  const int wg = blockIdx.x;
   const int xcd = wg & 7, slot = wg >> 3;
   const int per = total >> 3, rem = total & 7;
   const int t = xcd * per + min(xcd, rem) + slot;
@@ -179,7 +183,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
 
   const T* A = reinterpret_cast<const T*>(p.a);
   const T* Bw = reinterpret_cast<const T*>(p.b);
-  const int64_t rows_a = min<int64_t>(BM, p.M - m0);
+  const int64_t rows_a = min<int64_t>(BM, m_end - m0);
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + m0 * K, rows_a * K * 2);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bw + (int64_t)n0 * K, (int64_t)BN * K * 2);
 
@@ -322,7 +326,7 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int64_t m = m0 + wm * (BM / 2) + i * 32 + r32;
-    if (m >= p.M) continue;
+    if (m >= m_end) continue;
     const int64_t b = m / rpb;
     const int64_t within = m - b * rpb;
     const int64_t crow = b * p.c_map.batch_stride + p.c_map.row_offset + within;
@@ -379,15 +383,63 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t m
 // second launch behind the first costs about 3072/K waves (its start-up and
 // the first launch's drain, measured at roughly 50 us).  E.g. 17776 x 3072 x
 // 12288: 840 tiles = 4 waves, or 768 + 132 half tiles = 3 + 0.62 + 0.25.
-static int64_t gemm_row_split(int64_t M, int tiles_n, int K) {
-  constexpr int CUS = 256;
-  auto waves = [&](int64_t tiles) { return (double)((tiles + CUS - 1) / CUS); };
+// One launch, two tile heights: workgroups below tiles_big take 256-row
+// tiles of rows [0, split), the rest 128-row tiles of rows [split, M).  The
+// half-height tiles come last in dispatch order and fill the CUs the last
+// round of full tiles leaves idle.
+template <typename T, int EPI, typename CT, typename RT>
+__global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t split, int tiles_big,
+                                                         const uint16_t* __restrict__ bias,
+                                                         CT* __restrict__ cout,
+                                                         const RT* __restrict__ resid,
+                                                         const float* __restrict__ gate) {
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS * (256 * BK * 2 + B_BYTES)];
+  if ((int)blockIdx.x < tiles_big)
+    gemm_tile<T, EPI, CT, RT, 256>(p, 0, split, (int)blockIdx.x, smem, bias, cout, resid, gate);
+  else
+    gemm_tile<T, EPI, CT, RT, 128>(p, split, p.M, (int)blockIdx.x - tiles_big, smem, bias, cout, resid,
+                                   gate);
+}
+
+// Completion time of n_big full tiles, then n_small half-height tiles costing
+// `half` of a full one, dealt in order to the first free of 256 CUs (tiles
+// freed at the same time form one group).
+static double tile_makespan(int64_t n_big, int64_t n_small, double half) {
+  constexpr int64_t CUS = 256;
+  const int64_t rounds = n_big / CUS, extra = n_big % CUS;
+  std::vector<std::pair<double, int64_t>> free_at;  // (time, CUs)
+  if (CUS - extra) free_at.push_back({(double)rounds, CUS - extra});
+  if (extra) free_at.push_back({(double)rounds + 1.0, extra});
+  double end = free_at.back().first;
+  if (n_big == 0) end = 0.0;
+  while (n_small > 0) {
+    size_t i = 0;
+    for (size_t j = 1; j < free_at.size(); ++j)
+      if (free_at[j].first < free_at[i].first) i = j;
+    const double t = free_at[i].first;
+    const int64_t k = std::min(free_at[i].second, n_small);
+    n_small -= k;
+    end = std::max(end, t + half);
+    if (free_at[i].second == k) free_at.erase(free_at.begin() + i);
+    else free_at[i].second -= k;
+    bool merged = false;
+    for (auto& g : free_at)
+      if (g.first == t + half) { g.second += k; merged = true; }
+    if (!merged) free_at.push_back({t + half, k});
+  }
+  return end;
+}
+
+// Rows [0, split) go to 256-row tiles, the rest to 128-row tiles: the split
+// with the least modelled completion time, a half-height tile costing 0.62 of
+// a full one (measured).  Small M runs 128-row tiles only.
+static int64_t gemm_row_split(int64_t M, int tiles_n) {
   const int64_t tm = (M + 255) / 256;
   int64_t best_split = M;
-  double best = waves(tm * tiles_n);
+  double best = tile_makespan(tm * tiles_n, 0, 0.62);
   for (int64_t t1 = tm - 1; t1 >= 0 && t1 >= tm - 16; --t1) {
     const int64_t rest = (M - t1 * 256 + 127) / 128;
-    const double cost = waves(t1 * tiles_n) + 0.62 * waves(rest * tiles_n) + (t1 > 0 ? 3072.0 / K : 0.0);
+    const double cost = tile_makespan(t1 * tiles_n, rest * tiles_n, 0.62);
     if (cost < best - 1e-9) { best = cost; best_split = t1 * 256; }
   }
   return best_split;
@@ -396,19 +448,11 @@ static int64_t gemm_row_split(int64_t M, int tiles_n, int K) {
 template <typename T, int EPI, typename CT, typename RT>
 static hipError_t launch_t(const GemmParams& p, hipStream_t s) {
   const int tiles_n = p.N / BN;
-  const int64_t split = gemm_row_split(p.M, tiles_n, p.K);
-  if (split > 0) {
-    const int64_t tiles = ((split + 255) / 256) * tiles_n;
-    GemmParams q = p;
-    q.M = split;
-    hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT, 256>), dim3((unsigned)tiles), dim3(NWAVES * 64), 0, s,
-                       q, (int64_t)0, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
-  }
-  if (split < p.M) {
-    const int64_t tiles = ((p.M - split + 127) / 128) * tiles_n;
-    hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT, 128>), dim3((unsigned)tiles), dim3(NWAVES * 64), 0, s,
-                       p, split, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
-  }
+  const int64_t split = gemm_row_split(p.M, tiles_n);
+  const int64_t big = ((split + 255) / 256) * tiles_n;
+  const int64_t small = ((p.M - split + 127) / 128) * tiles_n;
+  hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT>), dim3((unsigned)(big + small)), dim3(NWAVES * 64), 0, s, p,
+                     split, (int)big, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
   return hipGetLastError();
 }
 
