@@ -74,9 +74,13 @@ def bench_gpu(args, shape):
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
 
+    # a chunked call runs each chunk's attention on a second stream, overlapping
+    # the previous chunk's projections (bit-identical to one stream)
+    aux = None if args.one_stream else torch.cuda.Stream()
+
     def step():
-        X.xema_dit_block_fwd_serial(cfg, req, x, weights, cond, group, plan.chunk_tokens, ws, ws.numel(), out,
-                                    stream)
+        X.xema_dit_block_fwd_pipelined(cfg, req, x, weights, cond, group, plan.chunk_tokens, ws, ws.numel(),
+                                       out, stream, aux if aux is not None else stream)
 
     for _ in range(args.warmup):
         step()
@@ -429,6 +433,8 @@ def main():
                     help="device weight budget in bytes; the plan picks the smallest K (step mode)")
     ap.add_argument("--staging", type=int, default=2, help="device staging slots (step mode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--one-stream", action="store_true",
+                    help="run chunked phase B on one stream (no attention/projection overlap)")
     ap.add_argument("--vae", default=None, help="time the VAE upsampling stage vae_video or vae_1080p instead")
     ap.add_argument("--vae-torch-context", action="store_true",
                     help="with --vae, also time the stage unfused through PyTorch (context only)")
@@ -481,6 +487,7 @@ def main():
             "batch": B, "seq_len": L, "hidden": shape.hidden, "heads": H, "head_dim": d,
             "mlp_hidden": shape.mlp_hidden, "flops_per_step": flops,
             "budget_bytes": args.budget, "chunk_tokens": plan.chunk_tokens, "batch_group": g["batch_group"],
+            "phase_b_streams": 1 if args.one_stream or plan.chunk_tokens >= shape.seq_len else 2,
             "arena_bytes": plan.workspace_bytes, "device_peak_bytes": g["device_peak_bytes"],
         },
         "roofline": {

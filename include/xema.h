@@ -103,7 +103,7 @@ typedef struct {
   int32_t chunk_tokens;               /* tokens per sequence per chunk; == L means unchunked */
   int32_t n_slots;
   int64_t workspace_bytes;            /* arena size at chunk_tokens (Algorithm 1 peak) */
-  int64_t min_workspace_bytes;        /* arena size at the smallest candidate chunk */
+  int64_t min_workspace_bytes;        /* the smallest arena over the candidate chunks */
   int64_t slot_offset[XEMA_MAX_SLOTS];
   int64_t slot_bytes[XEMA_MAX_SLOTS];
   int32_t slot_begin[XEMA_MAX_SLOTS];
@@ -125,7 +125,8 @@ enum {
   XEMA_SLOT_WO16,      /* fp16 [D, D]                        life [4, 10) */
   XEMA_SLOT_WUP16,     /* fp16 [F, D]                        life [4, 10) */
   XEMA_SLOT_WDOWN16,   /* fp16 [D, F]                        life [4, 10) */
-  XEMA_SLOT_ATTN,      /* fp16 [B*c, D]                      life [5, 7)  */
+  XEMA_SLOT_ATTN,      /* fp16 [B*c, D]      life [5, 7); [5, 10) when chunked (the
+                          next chunk's attention may overlap this chunk's MLP) */
   XEMA_SLOT_X1,        /* fp32 [B*c, D]                      life [6, 10) */
   XEMA_SLOT_LN2,       /* fp16 [B*c, D]                      life [7, 9)  */
   XEMA_SLOT_HID,       /* fp16 [B*c, F]                      life [8, 10) */
@@ -158,7 +159,8 @@ XEMA_API int xema_workspace_bytes(const xema_block_cfg* cfg, const xema_request*
  * caller-owned tokens, weights, conditioning and output are not in it.
  * Host only.
  * Errors: XEMA_ERR_BUDGET_TOO_SMALL when no candidate fits (out->chunk_tokens
- * is then 0 and out->min_workspace_bytes holds the smallest arena);
+ * is then 0 and out->min_workspace_bytes holds the smallest arena over the
+ * candidates);
  * XEMA_ERR_INVALID_ARG, XEMA_ERR_UNSUPPORTED.                              */
 XEMA_API int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* req,
                         int64_t budget_bytes, xema_plan* out);
@@ -224,6 +226,27 @@ XEMA_API int xema_dit_block_fwd_serial(const xema_block_cfg* cfg, const xema_req
                               const void* cond, int32_t batch_group, int32_t chunk_tokens,
                               void* workspace, int64_t workspace_bytes,
                               void* out, void* stream);
+
+/* xema_dit_block_fwd_serial with the attention of each query chunk on a
+ * second stream: with two chunks or more, the attention of chunk k runs on
+ * aux_stream as soon as the out-projection of chunk k-1 has read the
+ * attention buffer, alongside the LN2 and MLP of chunk k-1 on `stream`, so
+ * the last, partly filled round of workgroups of one kernel overlaps the
+ * other's (chunking should cost only what the budget needs, Sec. 5.1; this
+ * trims what a chunk too small to fill the GPU costs).  The chunked layout
+ * keeps the attention buffer apart from the MLP's buffers for this.  HIP
+ * events created and released by the call order the streams; the output is
+ * bit-identical to xema_dit_block_fwd.  aux_stream NULL or equal to
+ * `stream`, or an unchunked call, runs everything on `stream`.
+ * Asynchronous on `stream`: when work queued on `stream` after this call
+ * starts, the aux_stream work of this call has finished.  Calls that share a
+ * workspace must be ordered on `stream`; aux_stream must have the default
+ * priority.  Errors as xema_dit_block_fwd.                                 */
+XEMA_API int xema_dit_block_fwd_pipelined(const xema_block_cfg* cfg, const xema_request* req,
+                                 const void* tokens, const xema_block_weights* weights,
+                                 const void* cond, int32_t batch_group, int32_t chunk_tokens,
+                                 void* workspace, int64_t workspace_bytes,
+                                 void* out, void* stream, void* aux_stream);
 
 /* Static string naming a status code. */
 XEMA_API const char* xema_status_str(int status);

@@ -113,7 +113,9 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
     query chunk) 5 = attention, 6 = out-projection with gated residual, 7 = LN2,
     8 = MLP up + GELU, 9 = MLP down + gated residual.  Per-chunk slots are
     reused by every chunk; Q, K, V hold all tokens, padded to a multiple of
-    SEQ_PAD tokens.  A dual-stream block (reading R24) keeps both modulation
+    SEQ_PAD tokens.  In a chunked call the attention buffer stays live
+    through the chunk's MLP (steps 5-9), so the next chunk's attention may
+    run meanwhile on a second stream.  A dual-stream block (reading R24) keeps both modulation
     vectors, so its mod slot doubles."""
     B, D, F = batch, hidden, mlp_hidden
     c = seq_len if chunk <= 0 or chunk >= seq_len else chunk
@@ -129,7 +131,7 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
         ("wo16", 2 * D * D, 4, 10),
         ("wup16", 2 * F * D, 4, 10),
         ("wdown16", 2 * D * F, 4, 10),
-        ("attn", 2 * B * c * D, 5, 7),
+        ("attn", 2 * B * c * D, 5, 10 if c < seq_len else 7),
         ("x1", 4 * B * c * D, 6, 10),
         ("ln2", 2 * B * c * D, 7, 9),
         ("hid", 2 * B * c * F, 8, 10),
@@ -153,10 +155,10 @@ def chunk_candidates(seq_len: int) -> List[int]:
 
 def plan(shape, budget_bytes: int):
     """Largest candidate chunk whose arena fits `budget_bytes`.
-    Returns (chunk or None, arena bytes at that chunk, arena bytes at the
-    smallest candidate)."""
+    Returns (chunk or None, arena bytes at that chunk, the smallest arena over
+    the candidates)."""
     cands = chunk_candidates(shape.seq_len)
-    smallest = workspace_bytes(shape, cands[-1])
+    smallest = min(workspace_bytes(shape, c) for c in cands)
     for c in cands:
         ws = workspace_bytes(shape, c)
         if ws <= budget_bytes:

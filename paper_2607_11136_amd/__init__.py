@@ -148,6 +148,9 @@ _SIGNATURES = {
     "xema_dit_step_fwd": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
                                          ctypes.POINTER(BlockWeights), ctypes.POINTER(OffloadPlan),
                                          _P, _I32, _P, _I64, _P, _P, _P]),
+    "xema_dit_block_fwd_pipelined": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
+                                                    ctypes.POINTER(BlockWeights), _P, _I32, _I32, _P, _I64, _P,
+                                                    _P, _P]),
     "xema_vae_upconv_weight_bytes": (ctypes.c_int, [_I32, _I32, ctypes.POINTER(_I64)]),
     "xema_vae_upconv_prepare": (ctypes.c_int, [_P, _I32, _I32, _P, _P]),
     "xema_vae_upconv": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _I32, _I32, _I32, _P, _P]),
@@ -300,6 +303,16 @@ def xema_workspace_plan_serial(cfg: BlockCfg, req: Request, budget_bytes: int):
         e.plan = p
         raise e
     return g.value, p
+
+
+def xema_dit_block_fwd_pipelined(cfg: BlockCfg, req: Request, tokens, weights: BlockWeights, cond,
+                                 batch_group: int, chunk_tokens: int, workspace, workspace_bytes: int, out,
+                                 stream=None, aux_stream=None) -> None:
+    """xema_dit_block_fwd_serial with each chunk's attention on aux_stream."""
+    _check(lib().xema_dit_block_fwd_pipelined(ctypes.byref(cfg), ctypes.byref(req), _ptr(tokens),
+                                              ctypes.byref(weights), _ptr(cond), batch_group, chunk_tokens,
+                                              _ptr(workspace), int(workspace_bytes), _ptr(out), _stream(stream),
+                                              _stream(aux_stream)), "xema_dit_block_fwd_pipelined")
 
 
 def xema_dit_block_fwd_serial(cfg: BlockCfg, req: Request, tokens, weights: BlockWeights, cond,

@@ -219,7 +219,7 @@ namespace xema {
 // ch, out is [B, L, D] fp32.
 int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens, int x_dtype,
               const xema_block_weights& w, const void* cond, int64_t ch, uint8_t* ws,
-              const xema_plan& plan, float* out, hipStream_t s) {
+              const xema_plan& plan, float* out, hipStream_t s, hipStream_t aux) {
   const int64_t B = r.batch, L = seq_len(r), D = c.hidden, F = c.mlp_hidden, Dc = c.cond_dim;
   const int64_t Lp = padded_len(L);
   auto slot = [&](int id) { return (void*)(ws + plan.slot_offset[id]); };
@@ -279,31 +279,36 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
   XEMA_TRY(launch_convert_f16((const uint16_t*)w.down_w, (_Float16*)wdown16, D * F, s));
 
   // phase B: attention -> out-proj -> LN2 -> MLP, per query chunk
-  for (int64_t t0 = 0; t0 < L; t0 += ch) {
-    const int64_t cc = std::min(ch, L - t0);
-    const RowMap ident{cc, cc, 0};
+  auto attention_of = [&](int64_t t0, void* dst, hipStream_t q) {
     AttnParams ap;
     ap.q = (const _Float16*)Q; ap.k = (const _Float16*)Kk; ap.vt = (const _Float16*)VT;
-    ap.o = (_Float16*)attn; ap.batch = (int)B; ap.heads = c.heads; ap.seq_len = (int)L;
-    ap.padded_len = (int)Lp; ap.q_begin = (int)t0; ap.q_count = (int)cc;
-    XEMA_TRY(launch_attention(ap, c.head_dim, s));
-
+    ap.o = (_Float16*)dst; ap.batch = (int)B; ap.heads = c.heads; ap.seq_len = (int)L;
+    ap.padded_len = (int)Lp; ap.q_begin = (int)t0; ap.q_count = (int)std::min(ch, L - t0);
+    return launch_attention(ap, c.head_dim, q);
+  };
+  // the out-projection of the chunk at t0 (reading attention output src),
+  // then `used` (if any) is recorded, then LN2 and the MLP
+  auto projections_of = [&](int64_t t0, const void* src, hipEvent_t used) {
+    const int64_t cc = std::min(ch, L - t0);
+    const RowMap ident{cc, cc, 0};
     GemmParams g{};
-    g.dtype = XEMA_F16; g.a = attn; g.b = wo16; g.M = B * cc; g.N = (int)D; g.K = (int)D;
+    g.dtype = XEMA_F16; g.a = src; g.b = wo16; g.M = B * cc; g.N = (int)D; g.K = (int)D;
     g.bias = (const uint16_t*)w.o_b; g.epilogue = XEMA_EPI_GATED_RESIDUAL;
     g.c = x1; g.c_dtype = XEMA_F32; g.c_map = ident; g.ldc = D;
     g.resid = tokens; g.resid_dtype = x_dtype; g.resid_map = RowMap{cc, L, t0}; g.ld_resid = D;
     g.gate = mod + 2 * D; g.gate_stride = 6 * D; g.gate_sel = sel_at(t0);
-    XEMA_TRY(launch_gemm(g, s));
+    if (launch_gemm(g, s) != hipSuccess) return hipErrorLaunchFailure;
+    if (used && hipEventRecord(used, s) != hipSuccess) return hipErrorLaunchFailure;
 
-    XEMA_TRY(launch_ln_modulate(x1, XEMA_F32, ident, B * cc, (int)D, mod + 3 * D, mod + 4 * D,
-                                6 * D, sel_at(t0), c.ln_eps, ln2, XEMA_F16, s));
+    hipError_t e = launch_ln_modulate(x1, XEMA_F32, ident, B * cc, (int)D, mod + 3 * D, mod + 4 * D,
+                                      6 * D, sel_at(t0), c.ln_eps, ln2, XEMA_F16, s);
+    if (e != hipSuccess) return e;
 
     GemmParams u{};
     u.dtype = XEMA_F16; u.a = ln2; u.b = wup16; u.M = B * cc; u.N = (int)F; u.K = (int)D;
     u.bias = (const uint16_t*)w.up_b; u.epilogue = XEMA_EPI_BIAS_GELU;
     u.c = hid; u.c_dtype = XEMA_F16; u.c_map = ident; u.ldc = F;
-    XEMA_TRY(launch_gemm(u, s));
+    if ((e = launch_gemm(u, s)) != hipSuccess) return e;
 
     GemmParams d{};
     d.dtype = XEMA_F16; d.a = hid; d.b = wdown16; d.M = B * cc; d.N = (int)D; d.K = (int)F;
@@ -311,8 +316,44 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     d.c = out; d.c_dtype = XEMA_F32; d.c_map = RowMap{cc, L, t0}; d.ldc = D;
     d.resid = x1; d.resid_dtype = XEMA_F32; d.resid_map = ident; d.ld_resid = D;
     d.gate = mod + 5 * D; d.gate_stride = 6 * D; d.gate_sel = sel_at(t0);
-    XEMA_TRY(launch_gemm(d, s));
+    return launch_gemm(d, s);
+  };
+
+  const int64_t n_chunks = (L + ch - 1) / ch;
+  if (!aux || aux == s || n_chunks < 2) {
+    for (int64_t t0 = 0; t0 < L; t0 += ch) {
+      XEMA_TRY(attention_of(t0, attn, s));
+      XEMA_TRY(projections_of(t0, attn, nullptr));
+    }
+    return XEMA_OK;
   }
+
+  // Two streams: the attention of chunk k runs on `aux` once the
+  // out-projection of chunk k-1 has read the attention buffer, alongside the
+  // LN2 and MLP of chunk k-1 on `s`; one kernel's last, partly filled round
+  // overlaps the other's.  (The chunked layout keeps the attention buffer
+  // apart from x1, LN2 and the MLP's hidden buffer.)  Every operation and its
+  // inputs are those of the one-stream order, so the output is the same bit
+  // for bit.
+  hipEvent_t ev[3] = {};  // phase A done, attention done, buffer read
+  int made = 0;
+  auto finish = [&](int status) {
+    for (int i = 0; i < made; ++i) (void)hipEventDestroy(ev[i]);  // released once complete
+    return status;
+  };
+  for (; made < 3; ++made)
+    if (hipEventCreateWithFlags(&ev[made], hipEventDisableTiming) != hipSuccess) return finish(XEMA_ERR_HIP);
+  if (hipEventRecord(ev[0], s) != hipSuccess || hipStreamWaitEvent(aux, ev[0], 0) != hipSuccess)
+    return finish(XEMA_ERR_HIP);
+  for (int64_t k = 0; k < n_chunks; ++k) {
+    const int64_t t0 = k * ch;
+    if (k > 0 && hipStreamWaitEvent(aux, ev[2], 0) != hipSuccess) return finish(XEMA_ERR_HIP);
+    if (attention_of(t0, attn, aux) != hipSuccess || hipEventRecord(ev[1], aux) != hipSuccess ||
+        hipStreamWaitEvent(s, ev[1], 0) != hipSuccess)
+      return finish(XEMA_ERR_HIP);
+    if (projections_of(t0, attn, ev[2]) != hipSuccess) return finish(XEMA_ERR_HIP);
+  }
+  return finish(XEMA_OK);
 #undef XEMA_TRY
   return XEMA_OK;
 }
@@ -360,11 +401,10 @@ static int check_block_call(const xema_block_cfg* cfg, const xema_request* req, 
   return XEMA_OK;
 }
 
-extern "C" int xema_dit_block_fwd_serial(const xema_block_cfg* cfg, const xema_request* req,
-                                         const void* tokens, const xema_block_weights* w,
-                                         const void* cond, int32_t batch_group,
-                                         int32_t chunk_tokens, void* workspace,
-                                         int64_t workspace_bytes, void* out, void* stream) {
+static int block_fwd(const xema_block_cfg* cfg, const xema_request* req, const void* tokens,
+                     const xema_block_weights* w, const void* cond, int32_t batch_group,
+                     int32_t chunk_tokens, void* workspace, int64_t workspace_bytes, void* out,
+                     void* stream, void* aux_stream) {
   int st = check_block_call(cfg, req, tokens, w, cond, workspace, workspace_bytes, out);
   if (st != XEMA_OK) return st;
   if (batch_group < 1) return XEMA_ERR_INVALID_ARG;
@@ -388,16 +428,35 @@ extern "C" int xema_dit_block_fwd_serial(const xema_block_cfg* cfg, const xema_r
     const bool last = b0 + g >= B;
     st = run_block(c, last ? rl : rg, (const uint16_t*)tokens + b0 * L * D, XEMA_BF16, *w,
                    (const uint16_t*)cond + b0 * Dc, ch, (uint8_t*)workspace, last ? plan_l : plan_g,
-                   (float*)out + b0 * L * D, (hipStream_t)stream);
+                   (float*)out + b0 * L * D, (hipStream_t)stream, (hipStream_t)aux_stream);
     if (st != XEMA_OK) return st;
   }
   return XEMA_OK;
+}
+
+extern "C" int xema_dit_block_fwd_serial(const xema_block_cfg* cfg, const xema_request* req,
+                                         const void* tokens, const xema_block_weights* w,
+                                         const void* cond, int32_t batch_group,
+                                         int32_t chunk_tokens, void* workspace,
+                                         int64_t workspace_bytes, void* out, void* stream) {
+  return block_fwd(cfg, req, tokens, w, cond, batch_group, chunk_tokens, workspace, workspace_bytes, out,
+                   stream, nullptr);
 }
 
 extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* req,
                                   const void* tokens, const xema_block_weights* w,
                                   const void* cond, int32_t chunk_tokens, void* workspace,
                                   int64_t workspace_bytes, void* out, void* stream) {
-  return xema_dit_block_fwd_serial(cfg, req, tokens, w, cond, req ? req->batch : 1, chunk_tokens,
-                                   workspace, workspace_bytes, out, stream);
+  return block_fwd(cfg, req, tokens, w, cond, req ? req->batch : 1, chunk_tokens, workspace,
+                   workspace_bytes, out, stream, nullptr);
+}
+
+extern "C" int xema_dit_block_fwd_pipelined(const xema_block_cfg* cfg, const xema_request* req,
+                                            const void* tokens, const xema_block_weights* w,
+                                            const void* cond, int32_t batch_group,
+                                            int32_t chunk_tokens, void* workspace,
+                                            int64_t workspace_bytes, void* out, void* stream,
+                                            void* aux_stream) {
+  return block_fwd(cfg, req, tokens, w, cond, batch_group, chunk_tokens, workspace, workspace_bytes, out,
+                   stream, aux_stream);
 }

@@ -114,7 +114,9 @@ void block_weight_sizes(const xema_block_cfg& c, int64_t bytes[kWeightTensors]) 
 int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
                      xema_plan* out) {
   const int64_t B = req.batch, D = cfg.hidden, F = cfg.mlp_hidden;
-  const int64_t lp = padded_len(seq_len(req));
+  const int64_t L = seq_len(req);
+  const int64_t lp = padded_len(L);
+  const bool chunked = c < L;
   struct Spec { int64_t bytes; int begin, end; };
   const Spec spec[XEMA_NUM_SLOTS] = {
       {24 * B * D * (dual_stream(cfg) ? 2 : 1), 0, 10},  // XEMA_SLOT_MOD
@@ -127,7 +129,7 @@ int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t
       {2 * D * D, 4, 10},                          // XEMA_SLOT_WO16
       {2 * F * D, 4, 10},                          // XEMA_SLOT_WUP16
       {2 * D * F, 4, 10},                          // XEMA_SLOT_WDOWN16
-      {2 * B * c * D, 5, 7},                       // XEMA_SLOT_ATTN
+      {2 * B * c * D, 5, chunked ? 10 : 7},        // XEMA_SLOT_ATTN
       {4 * B * c * D, 6, 10},                      // XEMA_SLOT_X1
       {2 * B * c * D, 7, 9},                       // XEMA_SLOT_LN2
       {2 * B * c * F, 8, 10},                      // XEMA_SLOT_HID
@@ -190,6 +192,23 @@ extern "C" int xema_workspace_bytes(const xema_block_cfg* cfg, const xema_reques
   return rc;
 }
 
+namespace {
+
+// The smallest arena over the candidate chunks.  Usually the smallest chunk's,
+// but on short sequences a chunked layout (whose attention buffer stays live
+// through the MLP) can exceed the unchunked one.
+int64_t min_arena(const xema_block_cfg& cfg, const xema_request& req, const std::vector<int64_t>& cands) {
+  int64_t best = -1;
+  for (int64_t c : cands) {
+    xema_plan p;
+    layout_for_chunk(cfg, req, c, &p);
+    if (best < 0 || p.workspace_bytes < best) best = p.workspace_bytes;
+  }
+  return best;
+}
+
+}  // namespace
+
 extern "C" int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* req,
                                    int64_t budget_bytes, xema_plan* out) {
   if (!out) return XEMA_ERR_INVALID_ARG;
@@ -200,19 +219,18 @@ extern "C" int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request
   std::vector<int64_t> cands{L};
   for (int64_t c = (L - 1) / XEMA_CHUNK_GRANULE * XEMA_CHUNK_GRANULE; c > 0; c -= XEMA_CHUNK_GRANULE)
     cands.push_back(c);
-  xema_plan smallest;
-  layout_for_chunk(*cfg, *req, cands.back(), &smallest);
+  const int64_t smallest = min_arena(*cfg, *req, cands);
   for (int64_t c : cands) {
     xema_plan p;
     layout_for_chunk(*cfg, *req, c, &p);
     if (p.workspace_bytes <= budget_bytes) {
       *out = p;
-      out->min_workspace_bytes = smallest.workspace_bytes;
+      out->min_workspace_bytes = smallest;
       return XEMA_OK;
     }
   }
   std::memset(out, 0, sizeof(*out));
-  out->min_workspace_bytes = smallest.workspace_bytes;
+  out->min_workspace_bytes = smallest;
   return XEMA_ERR_BUDGET_TOO_SMALL;
 }
 
@@ -249,14 +267,13 @@ extern "C" int xema_workspace_plan_serial(const xema_block_cfg* cfg, const xema_
   }
   xema_request r1 = *req;
   r1.batch = 1;
-  xema_plan smallest;
-  layout_for_chunk(*cfg, r1, cands.back(), &smallest);
+  const int64_t smallest = min_arena(*cfg, r1, cands);
   if (*batch_group == 0) {
     std::memset(out, 0, sizeof(*out));
-    out->min_workspace_bytes = smallest.workspace_bytes;
+    out->min_workspace_bytes = smallest;
     return XEMA_ERR_BUDGET_TOO_SMALL;
   }
-  out->min_workspace_bytes = smallest.workspace_bytes;
+  out->min_workspace_bytes = smallest;
   return XEMA_OK;
 }
 

@@ -47,10 +47,12 @@ static_assert(sizeof(xema_block_weights) == kWeightTensors * sizeof(void*), "wei
 namespace xema {
 // One block forward on stream s (arguments validated by the caller): x is
 // [B, L, D] in x_dtype (XEMA_BF16 or XEMA_F32), the arena follows `plan`,
-// out is [B, L, D] fp32.
+// out is [B, L, D] fp32.  With a second stream `aux` (not null, not s) and
+// two chunks or more, each chunk's attention runs on aux, overlapping the
+// previous chunk's projections; the output is the same.
 int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens, int x_dtype,
               const xema_block_weights& w, const void* cond, int64_t ch, uint8_t* ws,
-              const xema_plan& plan, float* out, hipStream_t s);
+              const xema_plan& plan, float* out, hipStream_t s, hipStream_t aux = nullptr);
 }  // namespace xema
 #endif
 

@@ -35,7 +35,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = X.lib()
     declared = _declared_symbols()
-    assert len(declared) == 22, declared
+    assert len(declared) == 23, declared
     for name in declared:
         assert hasattr(lib, name), name
     assert declared == set(X.EXPORTED)
@@ -68,18 +68,25 @@ def test_layout_matches_oracle(name):
 @pytest.mark.parametrize("name", ["tiny", "video", "highres", "long"])
 def test_plan_matches_oracle(name):
     s = W.CONFIGS[name]
-    smallest = OL.workspace_bytes(s, OL.chunk_candidates(s.seq_len)[-1])
+    smallest = min(OL.workspace_bytes(s, c) for c in OL.chunk_candidates(s.seq_len))
     full = OL.workspace_bytes(s, 0)
     for budget in sorted({smallest, smallest + 12345, (smallest + full) // 2, full - 1, full,
                           32 * 10**9}):
         c, ws, small = OL.plan(s, budget)
+        if c is None:   # a chunked arena can exceed the unchunked one on short sequences
+            with pytest.raises(X.XemaError) as e:
+                X.xema_workspace_plan(_cfg(s), _req(s), budget)
+            assert e.value.status == X.XEMA_ERR_BUDGET_TOO_SMALL
+            assert e.value.plan.min_workspace_bytes == small
+            continue
         p = X.xema_workspace_plan(_cfg(s), _req(s), budget)
         assert (p.chunk_tokens, p.workspace_bytes, p.min_workspace_bytes) == (c, ws, small)
 
 
 def test_plan_budget_too_small_reports_minimum():
     s = W.HIGHRES
-    smallest = OL.workspace_bytes(s, 256)
+    smallest = min(OL.workspace_bytes(s, c) for c in OL.chunk_candidates(s.seq_len))
+    assert smallest == OL.workspace_bytes(s, 256)   # Q, K, V dominate: the smallest chunk is the smallest arena
     with pytest.raises(X.XemaError) as e:
         X.xema_workspace_plan(_cfg(s), _req(s), smallest - 1)
     assert e.value.status == X.XEMA_ERR_BUDGET_TOO_SMALL
@@ -100,9 +107,10 @@ def test_serial_plan_matches_oracle(name):
     chunk, that fits; only when chunking alone cannot fit the whole batch."""
     s = W.CONFIGS[name]
     cfg, req = _cfg(s), _req(s)
-    full_min = OL.workspace_bytes(s, OL.chunk_candidates(s.seq_len)[-1])
+    cands = OL.chunk_candidates(s.seq_len)
+    full_min = min(OL.workspace_bytes(s, c) for c in cands)
     one = s.with_(batch=1)
-    one_min = OL.workspace_bytes(one, OL.chunk_candidates(s.seq_len)[-1])
+    one_min = min(OL.workspace_bytes(one, c) for c in cands)
     budgets = [OL.workspace_bytes(s, 0), full_min, full_min - 1, (full_min + one_min) // 2, one_min, one_min - 1]
     for budget in budgets:
         ref = OL.plan_serial(s, budget)

@@ -221,3 +221,43 @@ def test_workload_parity_sampled_rows(name, chunk, nrows):
         assert torch.equal(other, out)
     del dev
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_pipelined_chunks_are_bit_identical(name):
+    """Each chunk's attention on a second stream (events between the
+    streams) gives the one-stream bytes; back-to-back calls on one workspace
+    stay ordered."""
+    s = SMALL[name]
+    dev = _device(s)
+    base, _, _ = dev.run(0)
+    aux = torch.cuda.Stream()
+    L = s.seq_len
+    for chunk in sorted({64, 100, 1 + L // 3}):
+        if chunk >= L:
+            continue
+        plan = X.xema_workspace_layout(dev.cfg, dev.req, chunk)
+        assert plan.slots()["attn"][3] == 10   # live through the MLP when chunked
+        ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+        outs = [torch.empty_like(base) for _ in range(3)]
+        for o in outs:   # no synchronisation between the calls
+            X.xema_dit_block_fwd_pipelined(dev.cfg, dev.req, dev.x, dev.weights, dev.cond, s.batch, chunk, ws,
+                                           ws.numel(), o, None, aux)
+        torch.cuda.synchronize()
+        for o in outs:
+            assert torch.equal(o, base), (name, chunk)
+
+
+def test_pipelined_groups_are_bit_identical():
+    s = SMALL["d128_b3"]
+    dev = _device(s)
+    base, _, _ = dev.run(0)
+    aux = torch.cuda.Stream()
+    chunk = 100
+    plan = X.xema_workspace_layout(dev.cfg, X.request(1, s.text_len, *s.grid), chunk)
+    ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+    out = torch.empty_like(base)
+    X.xema_dit_block_fwd_pipelined(dev.cfg, dev.req, dev.x, dev.weights, dev.cond, 1, chunk, ws, ws.numel(),
+                                   out, None, aux)
+    torch.cuda.synchronize()
+    assert torch.equal(out, base)
