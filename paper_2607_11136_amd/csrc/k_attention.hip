@@ -23,13 +23,14 @@
 //     the row sum), two wave groups run offset by a phase over a 3-stage LDS
 //     ring so one group's softmax overlaps the other's MFMAs;
 //   k_attention_lazy (used at d = 64): two column blocks per wave (half the
-//     LDS reads per score), a 2-stage ring, and a trigger on the tile max
-//     exceeding the reference by TAU = 8 (v_max3 reductions), which leaves the
-//     exponentials out of the branch; row sums by v_dot2 as above.  The
-//     reference is subtracted by the MFMA: one more k-step multiplies a
-//     column of ones in the key operand by -mrow in the query operand (kept
-//     fp16-representable), which costs 4 MFMAs per tile instead of 64
-//     subtractions per lane.  Scores must stay below 2^16 in log2 units.
+//     LDS reads per score) and a 2-stage ring.  The reference is subtracted
+//     by the MFMA: one more k-step multiplies a column of ones in the key
+//     operand by -mrow in the query operand (kept fp16-representable), which
+//     costs 4 MFMAs per tile instead of 64 subtractions per lane.  P is then
+//     taken straight from the MFMA output, and the trigger is the same P sum
+//     as above, so the common path has no max reduction; the rare rescaling
+//     path finds the tile max and recomputes P.  Scores must stay below 2^16
+//     in log2 units.
 // Measured on the workloads' own Q/K/V, each is the faster one at its width.
 //
 // Keys are visited in one fixed ascending order of 64-key tiles, and every
@@ -55,8 +56,7 @@ namespace xema {
 namespace {
 
 constexpr int KV = 64;          // keys per tile
-constexpr float PMAX = 4096.0f; // bound on a tile's P sum before the max moves
-constexpr float TAU = 8.0f;     // lazy-max slack of k_attention_lazy, log2 units
+constexpr float PMAX = 4096.0f; // bound on a lane's P sum over a tile before the max moves
 
 // Whether the reference max enters through the score MFMA's accumulator input
 // (16 more VGPRs per query column) or is subtracted before the exponential.
@@ -257,36 +257,39 @@ __device__ __forceinline__ void tile_softmax(const f32x16 (&s)[2][QB], bool firs
 }
 
 // Online softmax of one tile for k_attention_lazy.  The scores arrive as
-// s - mrow (the extra k-step of tile_scores_ones), so the common path takes
-// P = 2^s straight from the MFMA output.  A column grows when its tile max
-// exceeds TAU (and on the first tile): mrow moves to the tile max, rounded to
-// fp16 because it feeds the MFMA, O and the row sum are rescaled, and the
-// tile's scores are shifted in place.  Columns that do not grow shift by 0
-// and scale by 1.0, so a query's result never depends on the others of its
-// wave.  The row sum is the v_dot2 sum of the packed P.
+// s - mrow (the extra k-step of tile_scores_ones), so the common path packs
+// P = 2^s straight from the MFMA output; its v_dot2 sum is the row sum.  A
+// column grows when the larger of its two lanes' sums exceeds PMAX (a P
+// that overflows fp16 makes its sum infinite, so it always grows) and on
+// the first tile: mrow moves to the tile max, rounded to fp16 because it
+// feeds the MFMA, O and the row sum are rescaled, and P is recomputed from
+// the scores shifted by the move.  Columns that do not grow shift by 0 and
+// scale by 1.0, which reproduces their P bit for bit, so a query's result
+// never depends on the others of its wave.
 template <int HD, int QB>
-__device__ __forceinline__ void tile_softmax_ones(f32x16 (&s)[2][QB], bool first,
+__device__ __forceinline__ void tile_softmax_ones(const f32x16 (&s)[2][QB], bool first,
                                                   WaveState<HD, QB>& st, f16x8 (&pf)[QB][2][2],
                                                   int hi) {
-  float mxs[QB];
+  float lsp[QB];
   bool grow_any = first;
 #pragma unroll
   for (int c = 0; c < QB; ++c) {
-    float mx = s[0][c][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][c][r]);
-    mxs[c] = pair_max(mx);
-    grow_any |= mxs[c] > TAU;
+    lsp[c] = exp_pack<false>(s[0][c], s[1][c], 0.f, pf[c]);
+    grow_any |= lsp[c] > PMAX;
   }
   if (__builtin_amdgcn_ballot_w64(grow_any)) {
 #pragma unroll
     for (int c = 0; c < QB; ++c) {
-      const bool grow = first || mxs[c] > TAU;
+      const bool grow = first || pair_max(lsp[c]) > PMAX;
+      float mx = s[0][c][0];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][c][r]);
+      mx = pair_max(mx);
       float shift = 0.f;
       if (grow) {
-        const float mnew = (float)(f16)(st.mrow[c] + mxs[c]);
+        const float mnew = (float)(f16)(st.mrow[c] + mx);
         shift = mnew - st.mrow[c];
         st.mrow[c] = mnew;
       }
@@ -296,17 +299,14 @@ __device__ __forceinline__ void tile_softmax_ones(f32x16 (&s)[2][QB], bool first
       for (int d = 0; d < HD / 32; ++d)
 #pragma unroll
         for (int r = 0; r < 16; ++r) st.oacc[c][d][r] *= alpha;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][c][r] -= shift;   // x - 0 = x for the others
+      lsp[c] = exp_pack<true>(s[0][c], s[1][c], shift, pf[c]);   // x - 0 = x for the others
       f16x8 mn = {};
       mn[0] = hi ? (f16)0.f : (f16)(-st.mrow[c]);
       st.mneg[c] = mn;
     }
   }
 #pragma unroll
-  for (int c = 0; c < QB; ++c) st.lrow[c] += exp_pack<false>(s[0][c], s[1][c], 0.f, pf[c]);
+  for (int c = 0; c < QB; ++c) st.lrow[c] += lsp[c];
 }
 
 // O^T += V^T P^T
@@ -514,10 +514,10 @@ __device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int 
 }
 
 // Variant for narrow heads (d = 64): no group offset, two query column
-// blocks per wave (halving the LDS reads per score), a two-stage ring, and a
-// lazy max that moves when a tile's max exceeds the one in use by more than
-// TAU (log2 units), detected with max3 reductions; P = 2^(s - mrow).
-// Measured faster than k_attention at d = 64, slower at d = 128.
+// blocks per wave (halving the LDS reads per score), a two-stage ring, the
+// reference max subtracted by the score MFMA and the P-sum trigger
+// evaluated on the common path's own exponentials.  Measured faster than
+// k_attention at d = 64, slower at d = 128.
 template <int HD, int QB, int NW>
 __global__ __launch_bounds__(NW * 64) void k_attention_lazy(AttnParams p) {
   constexpr int K_BYTES = KV * HD * 2;        // K tile bytes

@@ -257,17 +257,11 @@ def test_qk_norm_rope_matches_oracle(head_dim, rope_dims, grid, text_len):
     assert np.all(got[..., L:] == 0)
 
 
-@pytest.mark.parametrize("head_dim", [64, 128])
-@pytest.mark.parametrize("L,q0,qn,scale", [(300, 0, 300, 1.0), (1000, 129, 700, 1.0), (1025, 0, 1025, 4.0),
-                                             (64, 0, 64, 1.0), (1, 0, 1, 1.0)])
-def test_attention_matches_oracle(head_dim, L, q0, qn, scale):
-    B, H = 2, 3
+def _attention_case(qs, k, v, q0, qn, what):
+    """Run the attention op on queries pre-multiplied by log2(e)/sqrt(d)
+    (weights 2^(qs . k)) and compare with the oracle."""
+    B, H, L, head_dim = qs.shape
     Lp = X.padded_len(L)
-    g = _rng(L + head_dim)
-    # the op takes queries pre-multiplied by log2(e)/sqrt(d): weights 2^(qs . k)
-    qs = _f16(g.standard_normal((B, H, L, head_dim)) * (scale * LOG2E / np.sqrt(head_dim)))
-    k = _f16(g.standard_normal((B, H, L, head_dim)) * scale)
-    v = _f16(g.standard_normal((B, H, L, head_dim)))
     q = qs.astype(np.float64) * (np.sqrt(head_dim) / LOG2E)
     qd = torch.zeros((B, H, Lp, head_dim), dtype=torch.float16, device=DEV)
     kd = torch.zeros_like(qd)
@@ -284,7 +278,45 @@ def test_attention_matches_oracle(head_dim, L, q0, qn, scale):
         for h in range(H):
             ref[b, :, h] = O.attention(q[b, h, q0:q0 + qn], k[b, h].astype(np.float64),
                                        v[b, h].astype(np.float64))
-    _check_close(got, ref, 2.0 ** -9, 2e-3, f"attention d={head_dim} L={L} q=[{q0},{q0 + qn}) x{scale}")
+    _check_close(got, ref, 2.0 ** -9, 2e-3, what)
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+@pytest.mark.parametrize("L,q0,qn,scale", [(300, 0, 300, 1.0), (1000, 129, 700, 1.0), (1025, 0, 1025, 4.0),
+                                             (64, 0, 64, 1.0), (1, 0, 1, 1.0)])
+def test_attention_matches_oracle(head_dim, L, q0, qn, scale):
+    B, H = 2, 3
+    g = _rng(L + head_dim)
+    qs = _f16(g.standard_normal((B, H, L, head_dim)) * (scale * LOG2E / np.sqrt(head_dim)))
+    k = _f16(g.standard_normal((B, H, L, head_dim)) * scale)
+    v = _f16(g.standard_normal((B, H, L, head_dim)))
+    _attention_case(qs, k, v, q0, qn, f"attention d={head_dim} L={L} q=[{q0},{q0 + qn}) x{scale}")
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+@pytest.mark.parametrize("profile", ["jump", "climb", "spike"])
+def test_attention_rescaling(head_dim, profile):
+    """Score profiles (log2 units, key index j) that drive the lazy reference
+    max: "jump" lifts the last 129 keys by 7.5, so a tile's P sum crosses the
+    trigger and the 896 earlier keys still carry a few percent of the weight
+    (a wrong rescale factor shows); "climb" rises by 20 per 64-key tile, so
+    the reference moves on every tile and the unshifted P of the common path
+    overflows fp16 before the rescale recomputes it; "spike" puts one key 60
+    above the rest.  Every query sees the same profile through its first
+    coordinate; the others add a little noise."""
+    B, H = 1, 2
+    L = 1000 if profile == "climb" else 1025
+    j = np.arange(L, dtype=np.float64)
+    lift = {"jump": np.where(j >= 896, 7.5, 0.0),
+            "climb": 20.0 * np.floor(j / 64),
+            "spike": np.where(j == 700, 60.0, 0.0)}[profile]
+    g = _rng({"jump": 301, "climb": 302, "spike": 303}[profile] + head_dim)
+    qs = np.concatenate([np.ones((B, H, L, 1)), 0.02 * g.standard_normal((B, H, L, head_dim - 1))], axis=-1)
+    k = g.standard_normal((B, H, L, head_dim))
+    k[..., 0] = lift
+    qs, k = _f16(qs), _f16(k)
+    v = _f16(g.standard_normal((B, H, L, head_dim)))
+    _attention_case(qs, k, v, 0, L, f"attention d={head_dim} rescaling profile {profile}")
 
 
 def test_attention_queries_independent_of_range():
