@@ -31,26 +31,35 @@ __global__ __launch_bounds__(256) void k_adaln(const uint16_t* __restrict__ cond
     float acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-    for (int k = lane * 8; k < cond_dim; k += 512) {
-      const u32x4 wv = *reinterpret_cast<const u32x4*>(wrow + k);
-      float wf[8];
+    // four 16-byte weight slices in flight per lane before their FMAs
+    for (int k0 = lane * 8; k0 < cond_dim; k0 += 4 * 512) {
+      u32x4 wv[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        wf[2 * e] = __uint_as_float(wv[e] << 16);
-        wf[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
-      }
+      for (int u = 0; u < 4; ++u)
+        if (k0 + u * 512 < cond_dim) wv[u] = *reinterpret_cast<const u32x4*>(wrow + k0 + u * 512);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        if (i < nb) {
-          const u32x4 cv =
-              *reinterpret_cast<const u32x4*>(cond + (int64_t)(b0 + i) * cond_dim + k);
-          float s = acc[i];
+      for (int u = 0; u < 4; ++u) {
+        const int k = k0 + u * 512;
+        if (k >= cond_dim) break;
+        float wf[8];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            s = fmaf(wf[2 * e], __uint_as_float(cv[e] << 16), s);
-            s = fmaf(wf[2 * e + 1], __uint_as_float(cv[e] & 0xffff0000u), s);
+        for (int e = 0; e < 4; ++e) {
+          wf[2 * e] = __uint_as_float(wv[u][e] << 16);
+          wf[2 * e + 1] = __uint_as_float(wv[u][e] & 0xffff0000u);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if (i < nb) {
+            const u32x4 cv =
+                *reinterpret_cast<const u32x4*>(cond + (int64_t)(b0 + i) * cond_dim + k);
+            float s = acc[i];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              s = fmaf(wf[2 * e], __uint_as_float(cv[e] << 16), s);
+              s = fmaf(wf[2 * e + 1], __uint_as_float(cv[e] & 0xffff0000u), s);
+            }
+            acc[i] = s;
           }
-          acc[i] = s;
         }
       }
     }
@@ -66,8 +75,11 @@ __global__ __launch_bounds__(256) void k_adaln(const uint16_t* __restrict__ cond
 
 // ---------------------------------------------------------------------------
 // a1 / a6: LayerNorm + AdaLN modulation.  One wave per row; lane l owns
-// elements [s*256 + 4l, s*256 + 4l + 4) for s = 0 .. dim/256 - 1.  A row of
-// a dual-stream block picks its shift/scale by its sequence position (ModSel).
+// elements [s*64*E + E*l, s*64*E + E*l + E) for s = 0 .. dim/(64 E) - 1:
+// E = 8 for 16-bit rows whose width 512 divides (16-byte loads), else E = 4
+// (fp32 rows keep each load instruction on one contiguous KiB).  A row
+// of a dual-stream block picks its shift/scale by its sequence position
+// (ModSel).
 // ---------------------------------------------------------------------------
 template <typename XT>
 __device__ __forceinline__ void load4(const XT* p, float v[4]);
@@ -94,7 +106,31 @@ __device__ __forceinline__ void store4(YT* p, const float v[4]) {
   *reinterpret_cast<y4*>(p) = o;
 }
 
-template <typename XT, typename YT, int NS>
+// E consecutive elements (E = 4 or 8) to and from fp32
+template <typename XT, int E>
+__device__ __forceinline__ void load_e(const XT* p, float (&v)[E]) {
+  if constexpr (E == 8 && sizeof(XT) == 2) {
+    const u32x4 u = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = __uint_as_float(u[e] << 16);
+      v[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < E / 4; ++h) load4<XT>(p + 4 * h, v + 4 * h);
+  }
+}
+template <typename YT, int E>
+__device__ __forceinline__ void store_e(YT* p, const float (&v)[E]) {
+  typedef YT ye __attribute__((ext_vector_type(E)));
+  ye o;
+#pragma unroll
+  for (int e = 0; e < E; ++e) o[e] = from_f32<YT>(v[e]);
+  *reinterpret_cast<ye*>(p) = o;
+}
+
+template <typename XT, typename YT, int NS, int E>
 __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, RowMap xmap,
                                                      int64_t rows, int dim,
                                                      const float* __restrict__ shift,
@@ -108,19 +144,21 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
   const int64_t within = r - b * xmap.rows_per_batch;
   const int64_t src = b * xmap.batch_stride + xmap.row_offset + within;
   const XT* xr = x + src * dim;
-  float v[NS][4];
+  float v[NS][E];
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
-    load4<XT>(xr + i * 256 + lane * 4, v[i]);
-    s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+    load_e<XT, E>(xr + i * 64 * E + lane * E, v[i]);
+#pragma unroll
+    for (int h = 0; h < E / 4; ++h)
+      s += (v[i][4 * h] + v[i][4 * h + 1]) + (v[i][4 * h + 2] + v[i][4 * h + 3]);
   }
   const float mean = wave_sum(s) / (float)dim;
   float q = 0.f;
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < E; ++e) {
       v[i][e] -= mean;
       q = fmaf(v[i][e], v[i][e], q);
     }
@@ -133,13 +171,16 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
   YT* yr = y + r * dim;
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
-    const int c = i * 256 + lane * 4;
-    const f32x4 s4 = *reinterpret_cast<const f32x4*>(sc + c);
-    const f32x4 h4 = *reinterpret_cast<const f32x4*>(sh + c);
-    float o[4];
+    const int c = i * 64 * E + lane * E;
+    float o[E];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = fmaf(v[i][e] * rstd, 1.0f + s4[e], h4[e]);
-    store4<YT>(yr + c, o);
+    for (int h = 0; h < E / 4; ++h) {
+      const f32x4 s4 = *reinterpret_cast<const f32x4*>(sc + c + 4 * h);
+      const f32x4 h4 = *reinterpret_cast<const f32x4*>(sh + c + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[4 * h + e] = fmaf(v[i][4 * h + e] * rstd, 1.0f + s4[e], h4[e]);
+    }
+    store_e<YT, E>(yr + c, o);
   }
 }
 
@@ -345,11 +386,30 @@ static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, cons
                               const float* scale, int64_t mod_stride, ModSel sel, float eps, YT* y,
                               hipStream_t s) {
   const dim3 grid((unsigned)((rows + 3) / 4));
+  if constexpr (sizeof(XT) == 2) {
+    if (dim % 512 == 0) {
+      switch (dim / 512) {
+#define XEMA_LN_CASE(NS)                                                                        \
+  case NS:                                                                                      \
+    hipLaunchKernelGGL((k_ln_modulate<XT, YT, NS, 8>), grid, dim3(256), 0, s, x, m, rows, dim,   \
+                       shift, scale, mod_stride, sel, eps, y);                                  \
+    break;
+        XEMA_LN_CASE(1) XEMA_LN_CASE(2) XEMA_LN_CASE(3) XEMA_LN_CASE(4) XEMA_LN_CASE(5)
+        XEMA_LN_CASE(6) XEMA_LN_CASE(7) XEMA_LN_CASE(8) XEMA_LN_CASE(9) XEMA_LN_CASE(10)
+        XEMA_LN_CASE(11) XEMA_LN_CASE(12) XEMA_LN_CASE(13) XEMA_LN_CASE(14) XEMA_LN_CASE(15)
+        XEMA_LN_CASE(16)
+#undef XEMA_LN_CASE
+        default:
+          return hipErrorInvalidValue;
+      }
+      return hipGetLastError();
+    }
+  }
   switch (dim / 256) {
-#define XEMA_LN_CASE(NS)                                                                   \
-  case NS:                                                                                 \
-    hipLaunchKernelGGL((k_ln_modulate<XT, YT, NS>), grid, dim3(256), 0, s, x, m, rows, dim, \
-                       shift, scale, mod_stride, sel, eps, y);                             \
+#define XEMA_LN_CASE(NS)                                                                      \
+  case NS:                                                                                    \
+    hipLaunchKernelGGL((k_ln_modulate<XT, YT, NS, 4>), grid, dim3(256), 0, s, x, m, rows, dim, \
+                       shift, scale, mod_stride, sel, eps, y);                                \
     break;
     XEMA_LN_CASE(1) XEMA_LN_CASE(2) XEMA_LN_CASE(3) XEMA_LN_CASE(4) XEMA_LN_CASE(5)
     XEMA_LN_CASE(6) XEMA_LN_CASE(7) XEMA_LN_CASE(8) XEMA_LN_CASE(9) XEMA_LN_CASE(10)

@@ -53,9 +53,10 @@ def test_adaln_matches_oracle():
 
 @pytest.mark.parametrize("x_dtype,y_dtype", [(X.XEMA_BF16, X.XEMA_BF16), (X.XEMA_F32, X.XEMA_F16),
                                              (X.XEMA_BF16, X.XEMA_F16), (X.XEMA_F32, X.XEMA_BF16)])
-def test_ln_modulate_matches_oracle(x_dtype, y_dtype):
+@pytest.mark.parametrize("D", [768, 1024])    # 4 and 8 elements per lane
+def test_ln_modulate_matches_oracle(x_dtype, y_dtype, D):
     g = _rng(3)
-    B, L, D = 3, 77, 768
+    B, L = 3, 77
     s0, cnt = 20, 45                       # a chunk of each sequence
     xs = g.standard_normal((B, L, D)) * 2.0 + 0.5
     mod = g.standard_normal((B, 6 * D)).astype(np.float32)
@@ -76,7 +77,7 @@ def test_ln_modulate_matches_oracle(x_dtype, y_dtype):
     ref = np.concatenate([O.modulate(O.layer_norm(x64[b, s0:s0 + cnt], 1e-6), m64[b, 3 * D:4 * D],
                                      m64[b, 4 * D:5 * D]) for b in range(B)])
     rel = 2.0 ** -8 if y_dtype == X.XEMA_BF16 else 2.0 ** -10
-    _check_close(y.float().cpu().numpy(), ref, rel, 1e-4, "ln_modulate")
+    _check_close(y.float().cpu().numpy(), ref, rel, 1e-4, f"ln_modulate D={D}")
 
 
 def _gemm_case(dtype, M, N, K, epi, seed, chunked=False):
