@@ -258,20 +258,27 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
                           mod + txt_delta, s));
   XEMA_TRY(launch_rope_table(geom, c.rope_theta, rope, s));
 
-  // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk
+  // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk.  At head
+  // dim 64 the QKV GEMM's epilogue does the scatter itself (one head per
+  // wave), the qkv slot stays unused and the padding tokens are zeroed once.
+  const bool fused_heads = c.head_dim == 64;
   for (int64_t t0 = 0; t0 < L; t0 += ch) {
     const int64_t cc = std::min(ch, L - t0);
     const RowMap xmap{cc, L, t0};
     XEMA_TRY(launch_ln_modulate(tokens, x_dtype, xmap, B * cc, (int)D, mod, mod + D, 6 * D,
                                 sel_at(t0), c.ln_eps, ln1, XEMA_BF16, s));
+    const QkRopeArgs qa = qk_args(c, r, qkv, (int)t0, (int)cc, w.q_gamma, w.k_gamma, rope, Q, Kk, VT);
     GemmParams g{};
     g.dtype = XEMA_BF16; g.a = ln1; g.b = w.qkv_w; g.M = B * cc; g.N = (int)(3 * D); g.K = (int)D;
-    g.bias = (const uint16_t*)w.qkv_b; g.epilogue = XEMA_EPI_BIAS;
+    g.bias = (const uint16_t*)w.qkv_b; g.epilogue = fused_heads ? EPI_QKV_HEADS : XEMA_EPI_BIAS;
     g.c = qkv; g.c_dtype = XEMA_F16; g.c_map = RowMap{cc, cc, 0}; g.ldc = 3 * D;
+    g.qk = qa;
     XEMA_TRY(launch_gemm(g, s));
-    const QkRopeArgs qa = qk_args(c, r, qkv, (int)t0, (int)cc, w.q_gamma, w.k_gamma, rope, Q, Kk, VT);
-    XEMA_TRY(launch_qk_norm_rope(qa, c.head_dim, s));
+    if (!fused_heads) XEMA_TRY(launch_qk_norm_rope(qa, c.head_dim, s));
   }
+  if (fused_heads)
+    XEMA_TRY(launch_qkv_pad(qk_args(c, r, qkv, 0, 0, w.q_gamma, w.k_gamma, rope, Q, Kk, VT),
+                            c.head_dim, (int)L, s));
 
   // step 4: fp16 copies of the phase-B weights
   XEMA_TRY(launch_convert_f16((const uint16_t*)w.o_w, (_Float16*)wo16, D * D, s));

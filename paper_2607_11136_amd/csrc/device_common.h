@@ -38,6 +38,15 @@ __device__ __forceinline__ f16 from_f32<f16>(float x) { return (f16)x; }
 template <>
 __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 
+// x as an fp32 register value: the empty asm keeps the compiler from merging
+// the operation that produced x into a following fp16 conversion (a mixed
+// multiply-add rounds once, the operation then the conversion round twice),
+// which it may do in one instantiation of a kernel and not in another.
+__device__ __forceinline__ float as_rounded_f32(float x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // Butterfly sum over the 64 lanes of a wave (fixed pairing order, so every
 // lane ends with the same, run-to-run reproducible value).
 __device__ __forceinline__ float wave_sum(float v) {

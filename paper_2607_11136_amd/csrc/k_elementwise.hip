@@ -448,6 +448,36 @@ hipError_t launch_rope_table(RopeGeom g, float theta, float* table, hipStream_t 
   return hipGetLastError();
 }
 
+// Zeros for the padding tokens [L, Lp) of Q and K ([B, H, Lp, d]) and V^T
+// ([B, H, d, Lp]) when the QKV GEMM writes the heads itself; one workgroup
+// per (head, batch row).
+template <int HD>
+__global__ __launch_bounds__(256) void k_qkv_pad(QkRopeArgs a, int seq_len) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int64_t Lp = a.padded_len;
+  const int64_t hb = (int64_t)b * a.heads + h;
+  const int n = (int)(Lp - seq_len) * HD;
+  for (int i = threadIdx.x; i < n; i += 256) {
+    const int64_t t = seq_len + i / HD;
+    const int d = i % HD;
+    a.q[(hb * Lp + t) * HD + d] = (f16)0.f;
+    a.k[(hb * Lp + t) * HD + d] = (f16)0.f;
+    a.vt[(hb * HD + d) * Lp + t] = (f16)0.f;
+  }
+}
+
+hipError_t launch_qkv_pad(const QkRopeArgs& a, int head_dim, int seq_len, hipStream_t s) {
+  if (a.padded_len <= seq_len || a.heads <= 0 || a.batch <= 0) return hipSuccess;
+  const dim3 grid((unsigned)a.heads, (unsigned)a.batch);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(k_qkv_pad<64>, grid, dim3(256), 0, s, a, seq_len);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL(k_qkv_pad<128>, grid, dim3(256), 0, s, a, seq_len);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_qk_norm_rope(const QkRopeArgs& a, int head_dim, hipStream_t s) {
   const dim3 grid((unsigned)((a.count_ext + 63) / 64), (unsigned)a.heads, (unsigned)a.batch);
   if (head_dim == 64)

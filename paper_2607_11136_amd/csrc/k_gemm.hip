@@ -95,12 +95,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
                                            BUF_FLAGS);
 }
 
+// (every element is rounded from its fp32 value, in both tile heights alike)
 template <typename CT>
 __device__ __forceinline__ void store4(CT* p, const float v[4]) {
   typedef CT c4 __attribute__((ext_vector_type(4)));
   c4 o;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) o[e] = from_f32<CT>(v[e]);
+  for (int e = 0; e < 4; ++e) o[e] = from_f32<CT>(sizeof(CT) == 2 ? as_rounded_f32(v[e]) : v[e]);
   *reinterpret_cast<c4*>(p) = o;
 }
 
@@ -136,6 +137,145 @@ __device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
+}
+
+// sum of the values of lanes l and l^32 (both lanes get the same result)
+__device__ __forceinline__ float pair_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Epilogue of the QKV GEMM at head_dim 64 (EPI_QKV_HEADS): steps a2 and a3
+// fused.  256 divides D, so a tile's columns lie in one section (Q, K or V),
+// and a wave's 64 columns are one head.  Lane (r32, hi) holds, for each of
+// its rows, the head dims 32 j + 8 q + 4 hi + e (j < 2, q < 4, e < 4): half
+// of the head, the other half being in lane r32 + 32 (1 - hi).  Q and K:
+// v = acc + bias, RMS over the 64 dims, times gamma, the 3D RoPE rotation of
+// the pairs (2p, 2p+1) and, for Q, the softmax factor log2(e)/sqrt(d), then
+// one fp16 rounding; stored to [B, H, Lp, 64].  V: rounded to fp16 and
+// transposed through LDS into [B, H, 64, Lp], 8 tokens per 16-byte store.
+// Rows are the tokens tok_begin + (m mod rows_per_batch) of batch row
+// m / rows_per_batch; nothing is written for m >= m_end.
+template <int MI, int NJ, int BM>
+__device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f32x16 (&acc)[MI][NJ],
+                                                   int64_t m0, int64_t m_end, int n0, int wm, int wn,
+                                                   int lane, int wave, uint8_t* smem,
+                                                   const uint16_t* __restrict__ bias) {
+  static_assert(NJ == 2, "one 64-dim head per wave");
+  const QkRopeArgs& a = p.qk;
+  const int r32 = lane & 31, hi = lane >> 5;
+  const int D = a.heads * 64;
+  const int sect = n0 / D;
+  const int h = (n0 - sect * D) / 64 + wn;
+  const int64_t rpb = p.c_map.rows_per_batch;
+  const int64_t Lp = a.padded_len;
+  const int col0 = n0 + wn * 64 + 4 * hi;
+  float bv[NJ][4][4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) load4f<uint16_t>(bias + col0 + j * 32 + 8 * q, bv[j][q]);
+
+  if (sect < 2) {
+    const uint16_t* gam = sect == 0 ? a.q_gamma : a.k_gamma;
+    float g[NJ][4][4];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) load4f<uint16_t>(gam + 4 * hi + j * 32 + 8 * q, g[j][q]);
+    const float f = sect == 0 ? a.q_scale : 1.0f;
+    f16* dst = sect == 0 ? a.q : a.k;
+    // pair p of the head rotates on axis 0, 1 or 2 when it falls in that
+    // axis' range of the cumulative dims/2; table rows: axis-major, then position
+    const int np0 = a.geom.dims[0] / 2, np1 = a.geom.dims[1] / 2, np2 = a.geom.dims[2] / 2;
+    const int tb1 = a.geom.grid[0] * np0, tb2 = tb1 + a.geom.grid[1] * np1;
+    const int gw = max(a.geom.grid[2], 1), hw = max(a.geom.grid[1] * a.geom.grid[2], 1);
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int64_t m = m0 + wm * (BM / 2) + i * 32 + r32;
+      const bool valid = m < m_end;
+      const int64_t bb = valid ? m / rpb : 0;
+      const int tok = a.tok_begin + (int)(valid ? m - bb * rpb : 0);
+      float v[NJ][4][4];
+      float ss = 0.f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[j][q][e] = acc[i][j][4 * q + e] + bv[j][q][e];
+            ss = fmaf(v[j][q][e], v[j][q][e], ss);
+          }
+      ss = pair_sum(ss);
+      // 1/sqrt(mean + eps) with the hardware reciprocal square root (1 ulp)
+      const float r = __builtin_amdgcn_rsqf(ss * (1.0f / 64.0f) + a.qk_eps);
+      const int vi = tok - a.text_len;    // visual index; text tokens are not rotated
+      const bool vis = valid && vi >= 0;
+      const int pt = vis ? vi / hw : 0, py = vis ? (vi % hw) / gw : 0, pw = vis ? vi % gw : 0;
+      f16* row = dst + (((int64_t)bb * a.heads + h) * Lp + tok) * 64 + 4 * hi;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          f16x4 o;
+#pragma unroll
+          for (int e2 = 0; e2 < 2; ++e2) {
+            const int pr = 16 * j + 4 * q + 2 * hi + e2;
+            float2 cs = make_float2(1.f, 0.f);
+            int idx = -1;
+            if (pr < np0) idx = pt * np0 + pr;
+            else if (pr < np0 + np1) idx = tb1 + py * np1 + (pr - np0);
+            else if (pr < np0 + np1 + np2) idx = tb2 + pw * np2 + (pr - np0 - np1);
+            if (vis && idx >= 0) cs = a.table[idx];
+            const float u0 = v[j][q][2 * e2] * r * g[j][q][2 * e2];
+            const float u1 = v[j][q][2 * e2 + 1] * r * g[j][q][2 * e2 + 1];
+            o[2 * e2] = (f16)as_rounded_f32(fmaf(u0, cs.x, -u1 * cs.y) * f);
+            o[2 * e2 + 1] = (f16)as_rounded_f32(fmaf(u0, cs.y, u1 * cs.x) * f);
+          }
+          if (valid) *reinterpret_cast<f16x4*>(row + j * 32 + 8 * q) = o;
+        }
+    }
+    return;
+  }
+
+  // V: every wave has finished reading the operand stages before they hold
+  // the transposed blocks (16 KiB per wave at BM = 256)
+  constexpr int TPW = BM / 2;  // tokens of this wave's block
+  __syncthreads();
+  f16* lds = reinterpret_cast<f16*>(smem) + wave * 64 * TPW;   // [64 dims][TPW tokens]
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          lds[(32 * j + 8 * q + 4 * hi + e) * TPW + i * 32 + r32] =
+              (f16)as_rounded_f32(acc[i][j][4 * q + e] + bv[j][q][e]);
+  __syncthreads();
+  for (int it = lane; it < 64 * (TPW / 8); it += 64) {
+    const int d = it / (TPW / 8), g8 = it % (TPW / 8);
+    const int64_t mf = m0 + wm * TPW + g8 * 8;
+    if (mf >= m_end) continue;
+    const f16x8 vals = *reinterpret_cast<const f16x8*>(lds + d * TPW + g8 * 8);
+    const int64_t bb = mf / rpb, ii = mf - bb * rpb;
+    const int tok = a.tok_begin + (int)ii;
+    f16* vrow = a.vt + (((int64_t)bb * a.heads + h) * 64 + d) * Lp;
+    if (mf + 8 <= m_end && ii + 8 <= rpb && (tok & 7) == 0) {
+      *reinterpret_cast<f16x8*>(vrow + tok) = vals;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t m = mf + e;
+        if (m < m_end) {
+          const int64_t b2 = m / rpb;
+          a.vt[(((int64_t)b2 * a.heads + h) * 64 + d) * Lp + a.tok_begin + (m - b2 * rpb)] = vals[e];
+        }
+      }
+    }
+  }
 }
 
 }  // namespace
@@ -312,6 +452,11 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
   // before the workgroup can end
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 
+  if constexpr (EPI == EPI_QKV_HEADS) {
+    epilogue_qkv_heads<MI, NJ, BM>(p, acc, m0, m_end, n0, wm, wn, lane, wave, smem_raw, bias);
+    return;
+  }
+
   // Epilogue.  acc[i][j][r] = C[m][n] with m = m0 + wm*(BM/2) + i*32 + r32 and
   // n = n0 + wn*64 + j*32 + 8*(r/4) + 4*hi + r%4.  Every input of a row group
   // is loaded before any of its stores (the pointers are restrict), so the
@@ -480,6 +625,9 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
       if (rf) return launch_t<bf16, XEMA_EPI_GATED_RESIDUAL, float, float>(p, s);
       return launch_t<bf16, XEMA_EPI_GATED_RESIDUAL, float, uint16_t>(p, s);
     }
+    case EPI_QKV_HEADS:
+      if (h) return hipErrorInvalidValue;
+      return launch_t<bf16, EPI_QKV_HEADS, f16, float>(p, s);
     default:
       return hipErrorInvalidValue;
   }

@@ -59,7 +59,13 @@ struct GemmParams {
   const float* gate;
   int64_t gate_stride;
   ModSel gate_sel;  // per-row choice of the gate vector (positions within c_map's rows)
+  QkRopeArgs qk;    // EPI_QKV_HEADS: rows are tokens [qk.tok_begin, +c_map.rows_per_batch)
 };
+
+// Internal epilogue of the QKV GEMM at head_dim 64 (steps a2 + a3 in one
+// kernel): bias, QK-RMSNorm, 3D RoPE and the scatter into Q, K and V^T,
+// without the [tokens, 3D] intermediate.  Not accepted by xema_op_gemm.
+constexpr int EPI_QKV_HEADS = 3;
 
 struct AttnParams {
   const _Float16* q;
@@ -89,6 +95,8 @@ hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows
                               ModSel sel, float eps, void* y, int y_dtype, hipStream_t s);
 hipError_t launch_rope_table(RopeGeom g, float theta, float* table, hipStream_t s);
 hipError_t launch_qk_norm_rope(const QkRopeArgs& a, int head_dim, hipStream_t s);
+// Zeros for the padding tokens [L, Lp) of Q, K and V^T (all batch rows, heads).
+hipError_t launch_qkv_pad(const QkRopeArgs& a, int head_dim, int seq_len, hipStream_t s);
 hipError_t launch_convert_f16(const uint16_t* src, _Float16* dst, int64_t n, hipStream_t s);
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, int head_dim, hipStream_t s);
