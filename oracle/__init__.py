@@ -39,6 +39,9 @@ alike):
   R24 dual-stream modulation: a block may carry a second AdaLN map
       (ada_txt_w, ada_txt_b) whose split modulates the text tokens (positions
       below L_t); the visual tokens keep m; every other weight is shared
+  R28 the block's slot table follows the implementation's intermediates: at
+      head_dim 64 the QKV projection writes Q, K and V^T directly, so the
+      [tokens, 3D] qkv slot is empty (layout.block_tensors)
 
 Parity pins: see tests/test_oracle_pins.py and tests/test_layout_oracle.py.
 The conventions R2, R5, R6, R9-R11 are fixed by no value the paper prints, so

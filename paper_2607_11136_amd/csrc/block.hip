@@ -8,6 +8,7 @@
 //            table, once per call
 //   phase A  for each chunk of c tokens: LN1 (a1) -> QKV GEMM (a2) ->
 //            QK-RMSNorm + RoPE scatter (a3), filling Q, K, V^T for all tokens
+//            (a2 and a3 are one kernel at head_dim 64)
 //   step 4   fp16 copies of W_o, W_up, W_down
 //   phase B  for each chunk of c queries: attention over all keys (a4) ->
 //            out-projection + gated residual (a5) -> LN2 (a6) -> MLP up +

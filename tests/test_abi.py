@@ -52,7 +52,7 @@ def test_layout_matches_oracle(name):
     for chunk in sorted({0, 1, 64, 100, 256, 2048, 8192} | set(s.chunks)):
         p = X.xema_workspace_layout(_cfg(s), _req(s), chunk)
         ts = OL.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, chunk,
-                              s.modulation_streams)
+                              s.modulation_streams, s.head_dim)
         offs, peak = OL.static_layout(ts)
         assert p.n_slots == len(ts) == len(X.SLOT_NAMES)
         assert p.workspace_bytes == peak
