@@ -263,6 +263,9 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
   // dim 64 the QKV GEMM's epilogue does the scatter itself (one head per
   // wave), the qkv slot stays unused and the padding tokens are zeroed once.
   const bool fused_heads = c.head_dim == 64;
+  // the qkv slot is sized for the unfused path only (empty at head_dim 64)
+  if (!fused_heads && plan.slot_bytes[XEMA_SLOT_QKV] < 6 * B * std::min(ch, L) * D)
+    return XEMA_ERR_INVALID_ARG;
   for (int64_t t0 = 0; t0 < L; t0 += ch) {
     const int64_t cc = std::min(ch, L - t0);
     const RowMap xmap{cc, L, t0};
