@@ -185,11 +185,42 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
       for (int q = 0; q < 4; ++q) load4f<uint16_t>(gam + 4 * hi + j * 32 + 8 * q, g[j][q]);
     const float f = sect == 0 ? a.q_scale : 1.0f;
     f16* dst = sect == 0 ? a.q : a.k;
-    // pair p of the head rotates on axis 0, 1 or 2 when it falls in that
-    // axis' range of the cumulative dims/2; table rows: axis-major, then position
-    const int np0 = a.geom.dims[0] / 2, np1 = a.geom.dims[1] / 2, np2 = a.geom.dims[2] / 2;
-    const int tb1 = a.geom.grid[0] * np0, tb2 = tb1 + a.geom.grid[1] * np1;
-    const int gw = max(a.geom.grid[2], 1), hw = max(a.geom.grid[1] * a.geom.grid[2], 1);
+    // (cos, sin) of the tile's BM tokens x 32 pairs, shared by its four heads:
+    // [BM][32] float2 rows padded to 272 bytes (conflict-free 16-byte reads
+    // by 16 consecutive rows), after [BM] int4 (valid, t, y, w) per token.
+    // Pair p of a head rotates on axis 0, 1 or 2 when it falls in that
+    // axis' range of the cumulative dims/2 (table: axis-major, then position).
+    constexpr int CS_STRIDE = 34;  // float2 per padded row
+    int4* pos_lds = reinterpret_cast<int4*>(smem);
+    float2* cs_lds = reinterpret_cast<float2*>(smem + BM * 16);
+    __syncthreads();  // every wave is done reading the operand stages
+    {
+      const int gw = max(a.geom.grid[2], 1), hw = max(a.geom.grid[1] * a.geom.grid[2], 1);
+      for (int t = (int)threadIdx.x; t < BM; t += NWAVES * 64) {
+        const int64_t m = m0 + t;
+        const bool valid = m < m_end;
+        const int64_t bb = valid ? m / rpb : 0;
+        const int vi = a.tok_begin + (int)(valid ? m - bb * rpb : 0) - a.text_len;
+        const bool vis = valid && vi >= 0;
+        pos_lds[t] = make_int4(vis ? 1 : 0, vis ? vi / hw : 0, vis ? (vi % hw) / gw : 0,
+                               vis ? vi % gw : 0);
+      }
+    }
+    __syncthreads();
+    {
+      const int np0 = a.geom.dims[0] / 2, np1 = a.geom.dims[1] / 2, np2 = a.geom.dims[2] / 2;
+      const int tb1 = a.geom.grid[0] * np0, tb2 = tb1 + a.geom.grid[1] * np1;
+      for (int e = (int)threadIdx.x; e < BM * 32; e += NWAVES * 64) {
+        const int t = e >> 5, pr = e & 31;
+        const int4 ps = pos_lds[t];
+        int idx = -1;
+        if (pr < np0) idx = ps.y * np0 + pr;
+        else if (pr < np0 + np1) idx = tb1 + ps.z * np1 + (pr - np0);
+        else if (pr < np0 + np1 + np2) idx = tb2 + ps.w * np2 + (pr - np0 - np1);
+        cs_lds[t * CS_STRIDE + pr] = (ps.x && idx >= 0) ? a.table[idx] : make_float2(1.f, 0.f);
+      }
+    }
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
       const int64_t m = m0 + wm * (BM / 2) + i * 32 + r32;
@@ -210,24 +241,18 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
       ss = pair_sum(ss);
       // 1/sqrt(mean + eps) with the hardware reciprocal square root (1 ulp)
       const float r = __builtin_amdgcn_rsqf(ss * (1.0f / 64.0f) + a.qk_eps);
-      const int vi = tok - a.text_len;    // visual index; text tokens are not rotated
-      const bool vis = valid && vi >= 0;
-      const int pt = vis ? vi / hw : 0, py = vis ? (vi % hw) / gw : 0, pw = vis ? vi % gw : 0;
+      const float2* csr = cs_lds + (wm * (BM / 2) + i * 32 + r32) * CS_STRIDE + 2 * hi;
       f16* row = dst + (((int64_t)bb * a.heads + h) * Lp + tok) * 64 + 4 * hi;
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
+          // pairs 16 j + 4 q + 2 hi + (0, 1)
+          const f32x4 cc = *reinterpret_cast<const f32x4*>(csr + 16 * j + 4 * q);
           f16x4 o;
 #pragma unroll
           for (int e2 = 0; e2 < 2; ++e2) {
-            const int pr = 16 * j + 4 * q + 2 * hi + e2;
-            float2 cs = make_float2(1.f, 0.f);
-            int idx = -1;
-            if (pr < np0) idx = pt * np0 + pr;
-            else if (pr < np0 + np1) idx = tb1 + py * np1 + (pr - np0);
-            else if (pr < np0 + np1 + np2) idx = tb2 + pw * np2 + (pr - np0 - np1);
-            if (vis && idx >= 0) cs = a.table[idx];
+            const float2 cs = make_float2(cc[2 * e2], cc[2 * e2 + 1]);
             const float u0 = v[j][q][2 * e2] * r * g[j][q][2 * e2];
             const float u1 = v[j][q][2 * e2 + 1] * r * g[j][q][2 * e2 + 1];
             o[2 * e2] = (f16)as_rounded_f32(fmaf(u0, cs.x, -u1 * cs.y) * f);
