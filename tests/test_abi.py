@@ -274,6 +274,9 @@ def test_op_validation():
     g = X.gemm_args(X.XEMA_F16, f, 100, 256, f, 256, f, X.XEMA_EPI_GATED_RESIDUAL, f + (1 << 30),
                     X.XEMA_F16, 256, resid=f, ld_resid=256, gate=f)
     assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_UNSUPPORTED
+    # the fused QKV-heads epilogue (code 3) is internal to the block forward
+    g = X.gemm_args(X.XEMA_BF16, f, 100, 256, f, 256, f, 3, f + (1 << 30), X.XEMA_F16, 256)
+    assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_INVALID_ARG
     # LN: dim not a multiple of 256
     assert L.xema_op_ln_modulate(f, X.XEMA_BF16, X.rowmap(4, 4, 0), 4, 300, f, f, 1800, 1e-6, f,
                                  X.XEMA_BF16, None) == X.XEMA_ERR_UNSUPPORTED
