@@ -131,6 +131,11 @@ EDGE = {
                                 rope_dims=(32, 48, 48)),
     "short": W.tiny_shape(name="short", cfg_id=62, batch=2, text_len=5, grid=(1, 4, 8), hidden=512,
                           heads=8, head_dim=64, mlp_hidden=1024, cond_dim=512, rope_dims=(16, 24, 24)),
+    # head_dim 64 takes the QKV GEMM's fused heads epilogue: every token rotated,
+    # chunks of one token put each GEMM row in another batch element
+    "visual_only_d64": W.tiny_shape(name="visual_only_d64", cfg_id=63, batch=2, text_len=0, grid=(3, 5, 7),
+                                    hidden=256, heads=4, head_dim=64, mlp_hidden=512, cond_dim=256,
+                                    rope_dims=(16, 24, 24)),
 }
 
 
