@@ -105,6 +105,33 @@ __device__ __forceinline__ void store4(CT* p, const float v[4]) {
   *reinterpret_cast<c4*>(p) = o;
 }
 
+// Two 8-column groups of one row, held as halves by lanes l (columns 0..3 of
+// each group) and l^32 (columns 4..7): the lanes swap one half each, then the
+// low lane stores group 0 and the high lane group 1, 16 bytes apiece.  `g0`
+// points at group 0; a and b are this lane's halves of groups 0 and 1.
+template <typename CT>
+__device__ __forceinline__ void store_group_pair(CT* g0, const CT __attribute__((ext_vector_type(4))) a,
+                                                 const CT __attribute__((ext_vector_type(4))) b, int hi,
+                                                 bool valid) {
+  typedef CT c4 __attribute__((ext_vector_type(4)));
+  typedef CT c8 __attribute__((ext_vector_type(8)));
+  static_assert(sizeof(c4) == 8, "16-bit elements");
+  const u32x2 send = __builtin_bit_cast(u32x2, hi ? a : b);
+  const auto r0 = __builtin_amdgcn_permlane32_swap(send[0], send[0], false, false);
+  const auto r1 = __builtin_amdgcn_permlane32_swap(send[1], send[1], false, false);
+  u32x2 got;  // the other lane's half: r[0] is the low lane's value, r[1] the high lane's
+  got[0] = hi ? r0[0] : r0[1];
+  got[1] = hi ? r1[0] : r1[1];
+  const c4 other = __builtin_bit_cast(c4, got);
+  c8 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    o[e] = hi ? other[e] : a[e];
+    o[4 + e] = hi ? b[e] : other[e];
+  }
+  if (valid) *reinterpret_cast<c8*>(g0 + 8 * hi) = o;
+}
+
 template <typename RT>
 __device__ __forceinline__ void load4f(const RT* p, float v[4]);
 template <>
@@ -242,24 +269,26 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
       // 1/sqrt(mean + eps) with the hardware reciprocal square root (1 ulp)
       const float r = __builtin_amdgcn_rsqf(ss * (1.0f / 64.0f) + a.qk_eps);
       const float2* csr = cs_lds + (wm * (BM / 2) + i * 32 + r32) * CS_STRIDE + 2 * hi;
-      f16* row = dst + (((int64_t)bb * a.heads + h) * Lp + tok) * 64 + 4 * hi;
+      f16* row = dst + (((int64_t)bb * a.heads + h) * Lp + tok) * 64;
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
+      for (int j = 0; j < NJ; ++j) {
+        f16x4 o[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           // pairs 16 j + 4 q + 2 hi + (0, 1)
           const f32x4 cc = *reinterpret_cast<const f32x4*>(csr + 16 * j + 4 * q);
-          f16x4 o;
 #pragma unroll
           for (int e2 = 0; e2 < 2; ++e2) {
             const float2 cs = make_float2(cc[2 * e2], cc[2 * e2 + 1]);
             const float u0 = v[j][q][2 * e2] * r * g[j][q][2 * e2];
             const float u1 = v[j][q][2 * e2 + 1] * r * g[j][q][2 * e2 + 1];
-            o[2 * e2] = (f16)as_rounded_f32(fmaf(u0, cs.x, -u1 * cs.y) * f);
-            o[2 * e2 + 1] = (f16)as_rounded_f32(fmaf(u0, cs.y, u1 * cs.x) * f);
+            o[q][2 * e2] = (f16)as_rounded_f32(fmaf(u0, cs.x, -u1 * cs.y) * f);
+            o[q][2 * e2 + 1] = (f16)as_rounded_f32(fmaf(u0, cs.y, u1 * cs.x) * f);
           }
-          if (valid) *reinterpret_cast<f16x4*>(row + j * 32 + 8 * q) = o;
         }
+#pragma unroll
+        for (int q = 0; q < 4; q += 2) store_group_pair<f16>(row + j * 32 + 8 * q, o[q], o[q + 1], hi, valid);
+      }
     }
     return;
   }
@@ -538,11 +567,27 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[j][q][e] = gelu_tanh(v[j][q][e]);
     }
+    if constexpr (sizeof(CT) == 2) {
+      typedef CT c4 __attribute__((ext_vector_type(4)));
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        store4<CT>(crow_ptr + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, v[j][q]);
+        for (int q = 0; q < 4; q += 2) {
+          c4 a, b;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            a[e] = from_f32<CT>(as_rounded_f32(v[j][q][e]));
+            b[e] = from_f32<CT>(as_rounded_f32(v[j][q + 1][e]));
+          }
+          store_group_pair<CT>(crow_ptr + n0 + wn * WN + j * 32 + 8 * q, a, b, hi, true);
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          store4<CT>(crow_ptr + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, v[j][q]);
+    }
   }
 }
 
