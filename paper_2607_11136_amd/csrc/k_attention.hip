@@ -29,8 +29,9 @@
 //     costs 4 MFMAs per tile instead of 64 subtractions per lane.  P is then
 //     taken straight from the MFMA output, and the trigger is the same P sum
 //     as above, so the common path has no max reduction; the rare rescaling
-//     path finds the tile max and recomputes P.  Scores must stay below 2^16
-//     in log2 units.
+//     path finds the tile max and recomputes P.  The two columns run offset
+//     within a tile, so that MFMAs of one are issued beside the
+//     exponentials of the other.  Scores must stay below 2^16 in log2 units.
 // Measured on the workloads' own Q/K/V, each is the faster one at its width.
 //
 // Keys are visited in one fixed ascending order of 64-key tiles, and every
@@ -152,12 +153,13 @@ struct WaveState {
   f16x8 mneg[QB];            // B fragment of the extra k-step: -mrow at k = 0
 };
 
-// S^T - mrow for two 32-key blocks x QB query columns: the score MFMAs plus
+// S^T - mrow for two 32-key blocks of one query column: the score MFMAs plus
 // one k-step of (a column of ones) x (-mrow), so the scores arrive shifted.
-template <int HD, int QB>
-__device__ __forceinline__ void tile_scores_ones(const uint8_t* Ks, const f16x8 (&qf)[QB][HD / 16],
-                                                 const f16x8 (&mneg)[QB], f16x8 ones, int krow,
-                                                 int kswz, int hi, f32x16 (&s)[2][QB]) {
+// (The key fragments are the same for every column; the compiler reads them
+// from LDS once per tile.)
+template <int HD>
+__device__ __forceinline__ void scores_col(const uint8_t* Ks, const f16x8 (&qc)[HD / 16], f16x8 mneg,
+                                           f16x8 ones, int krow, int kswz, int hi, f32x16 (&s)[2]) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int row = kb * 32 + krow;
@@ -165,11 +167,9 @@ __device__ __forceinline__ void tile_scores_ones(const uint8_t* Ks, const f16x8 
     for (int kk = 0; kk < HD / 16; ++kk) {
       const int slot16 = (kk * 2 + hi) ^ kswz;
       const f16x8 kf = *reinterpret_cast<const f16x8*>(Ks + row * (HD * 2) + slot16 * 16);
-#pragma unroll
-      for (int c = 0; c < QB; ++c) s[kb][c] = mma(kf, qf[c][kk], kk == 0 ? f32x16{} : s[kb][c]);
+      s[kb] = mma(kf, qc[kk], kk == 0 ? f32x16{} : s[kb]);
     }
-#pragma unroll
-    for (int c = 0; c < QB; ++c) s[kb][c] = mma(ones, mneg[c], s[kb][c]);
+    s[kb] = mma(ones, mneg, s[kb]);
   }
 }
 
@@ -206,6 +206,15 @@ __device__ __forceinline__ void mask_tail(f32x16 (&s)[2][QB], int tail, int hi) 
         for (int c = 0; c < QB; ++c) s[kb][c][r] = -INFINITY;
       }
     }
+}
+
+// the same for one query column
+__device__ __forceinline__ void mask_tail_col(f32x16 (&s)[2], int tail, int hi) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (kb * 32 + 16 * (r >> 3) + 8 * hi + (r & 7) >= tail) s[kb][r] = -INFINITY;
 }
 
 // Online softmax of one tile with a lazy reference max.  Scores arrive as
@@ -256,57 +265,42 @@ __device__ __forceinline__ void tile_softmax(const f32x16 (&s)[2][QB], bool firs
   for (int c = 0; c < QB; ++c) st.lrow[c] += lsp[c];
 }
 
-// Online softmax of one tile for k_attention_lazy.  The scores arrive as
-// s - mrow (the extra k-step of tile_scores_ones), so the common path packs
-// P = 2^s straight from the MFMA output; its v_dot2 sum is the row sum.  A
-// column grows when the larger of its two lanes' sums exceeds PMAX (a P
-// that overflows fp16 makes its sum infinite, so it always grows) and on
-// the first tile: mrow moves to the tile max, rounded to fp16 because it
-// feeds the MFMA, O and the row sum are rescaled, and P is recomputed from
-// the scores shifted by the move.  Columns that do not grow shift by 0 and
+// Online softmax for k_attention_lazy.  The scores arrive as s - mrow (the
+// extra k-step of scores_col), so the common path packs P = 2^s straight
+// from the MFMA output; its v_dot2 sum is the row sum.  A column grows when
+// the larger of its two lanes' sums exceeds PMAX (a P that overflows fp16
+// makes its sum infinite, so it always grows) and on the first tile; then
+// rescale_col moves mrow to the tile max, rounded to fp16 because it feeds
+// the MFMA, rescales O and the row sum, and recomputes P from the scores
+// shifted by the move.  Lanes whose column does not grow shift by 0 and
 // scale by 1.0, which reproduces their P bit for bit, so a query's result
 // never depends on the others of its wave.
 template <int HD, int QB>
-__device__ __forceinline__ void tile_softmax_ones(const f32x16 (&s)[2][QB], bool first,
-                                                  WaveState<HD, QB>& st, f16x8 (&pf)[QB][2][2],
-                                                  int hi) {
-  float lsp[QB];
-  bool grow_any = first;
+__device__ __forceinline__ void rescale_col(const f32x16 (&s)[2], bool first, int c, float& lsp,
+                                            WaveState<HD, QB>& st, f16x8 (&pfc)[2][2], int hi) {
+  const bool grow = first || pair_max(lsp) > PMAX;
+  float mx = s[0][0];
 #pragma unroll
-  for (int c = 0; c < QB; ++c) {
-    lsp[c] = exp_pack<false>(s[0][c], s[1][c], 0.f, pf[c]);
-    grow_any |= lsp[c] > PMAX;
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+  mx = pair_max(mx);
+  float shift = 0.f;
+  if (grow) {
+    const float mnew = (float)(f16)(st.mrow[c] + mx);
+    shift = mnew - st.mrow[c];
+    st.mrow[c] = mnew;
   }
-  if (__builtin_amdgcn_ballot_w64(grow_any)) {
+  const float alpha = first ? 0.f : (grow ? fast_exp2(-shift) : 1.f);
+  st.lrow[c] *= alpha;
 #pragma unroll
-    for (int c = 0; c < QB; ++c) {
-      const bool grow = first || pair_max(lsp[c]) > PMAX;
-      float mx = s[0][c][0];
+  for (int d = 0; d < HD / 32; ++d)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][c][r]);
-      mx = pair_max(mx);
-      float shift = 0.f;
-      if (grow) {
-        const float mnew = (float)(f16)(st.mrow[c] + mx);
-        shift = mnew - st.mrow[c];
-        st.mrow[c] = mnew;
-      }
-      const float alpha = first ? 0.f : (grow ? fast_exp2(-shift) : 1.f);
-      st.lrow[c] *= alpha;
-#pragma unroll
-      for (int d = 0; d < HD / 32; ++d)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) st.oacc[c][d][r] *= alpha;
-      lsp[c] = exp_pack<true>(s[0][c], s[1][c], shift, pf[c]);   // x - 0 = x for the others
-      f16x8 mn = {};
-      mn[0] = hi ? (f16)0.f : (f16)(-st.mrow[c]);
-      st.mneg[c] = mn;
-    }
-  }
-#pragma unroll
-  for (int c = 0; c < QB; ++c) st.lrow[c] += lsp[c];
+    for (int r = 0; r < 16; ++r) st.oacc[c][d][r] *= alpha;
+  lsp = exp_pack<true>(s[0], s[1], shift, pfc);   // x - 0 = x for the others
+  f16x8 mn = {};
+  mn[0] = hi ? (f16)0.f : (f16)(-st.mrow[c]);
+  st.mneg[c] = mn;
 }
 
 // O^T += V^T P^T
@@ -487,7 +481,10 @@ void k_attention(AttnParams p) {
 
 // One key tile of k_attention_lazy (tile kv in stage kv & 1; the next tile
 // is loaded into the other stage meanwhile).  LAST masks the keys at or past
-// `tail` and loads nothing.
+// `tail` and loads nothing.  The two query columns run offset: the score
+// MFMAs of column 1 are issued beside the exponentials of column 0, and the
+// P V^T MFMAs of column 0 beside those of column 1 (their V^T fragments are
+// kept for column 1).  Each column keeps its own order of operations.
 template <int HD, int QB, int NW, int K_INSTR, int V_INSTR, bool LAST>
 __device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int kv, int tail,
                                           __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
@@ -495,20 +492,51 @@ __device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int 
                                           const uint32_t (&v_off)[V_INSTR], int wave,
                                           const f16x8 (&qf)[QB][HD / 16], int krow, int kswz,
                                           int r32, int hi, WaveState<HD, QB>& st) {
+  static_assert(QB == 2, "two query column blocks per wave");
   constexpr int K_BYTES = KV * HD * 2;
   const int stage = kv & 1;
   if (!LAST)
     issue_kv<K_INSTR, V_INSTR, K_BYTES, NW>(rk, rv, k_off, v_off, smem[stage ^ 1], wave,
                                             (uint32_t)((kv + 1) * KV * HD * 2),
                                             (uint32_t)((kv + 1) * KV * 2));
-  f32x16 s[2][QB];
-  f16x8 pf[QB][2][2];
+  const uint8_t* Ks = smem[stage];
+  const uint8_t* Vs = smem[stage] + K_BYTES;
+  const bool first = kv == 0;
   f16x8 ones = {};
   ones[0] = hi ? (f16)0.f : (f16)1.f;
-  tile_scores_ones<HD, QB>(smem[stage], qf, st.mneg, ones, krow, kswz, hi, s);
-  if (LAST && tail < KV) mask_tail<QB>(s, tail, hi);
-  tile_softmax_ones<HD, QB>(s, kv == 0, st, pf, hi);
-  tile_pv<HD, QB>(smem[stage] + K_BYTES, pf, r32, hi, st.oacc);
+  f32x16 s0[2], s1[2];
+  f16x8 pf[QB][2][2];
+  scores_col<HD>(Ks, qf[0], st.mneg[0], ones, krow, kswz, hi, s0);
+  if (LAST && tail < KV) mask_tail_col(s0, tail, hi);
+  scores_col<HD>(Ks, qf[1], st.mneg[1], ones, krow, kswz, hi, s1);
+  float lsp0 = exp_pack<false>(s0[0], s0[1], 0.f, pf[0]);
+  if (__builtin_amdgcn_ballot_w64(first || lsp0 > PMAX))
+    rescale_col<HD, QB>(s0, first, 0, lsp0, st, pf[0], hi);
+  if (LAST && tail < KV) mask_tail_col(s1, tail, hi);
+  f16x8 vf[HD / 32][2][2];
+#pragma unroll
+  for (int d = 0; d < HD / 32; ++d) {
+    const int vrow = d * 32 + r32;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int slot16 = (kb * 4 + u * 2 + hi) ^ swz_v(vrow);
+        vf[d][kb][u] = *reinterpret_cast<const f16x8*>(Vs + vrow * (KV * 2) + slot16 * 16);
+        st.oacc[0][d] = mma(vf[d][kb][u], pf[0][kb][u], st.oacc[0][d]);
+      }
+  }
+  float lsp1 = exp_pack<false>(s1[0], s1[1], 0.f, pf[1]);
+  if (__builtin_amdgcn_ballot_w64(first || lsp1 > PMAX))
+    rescale_col<HD, QB>(s1, first, 1, lsp1, st, pf[1], hi);
+#pragma unroll
+  for (int d = 0; d < HD / 32; ++d)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) st.oacc[1][d] = mma(vf[d][kb][u], pf[1][kb][u], st.oacc[1][d]);
+  st.lrow[0] += lsp0;
+  st.lrow[1] += lsp1;
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 }
