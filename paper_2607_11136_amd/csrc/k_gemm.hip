@@ -31,8 +31,9 @@
 // output features of one token row: epilogue loads/stores are 8/16 bytes.
 //
 // Workgroups are dispatched round-robin over the 8 XCDs; the tile order
-// below gives each XCD a contiguous range of tiles, walked in groups of 8
-// tile-rows, so tiles that share operand panels share an L2.
+// below gives each XCD a contiguous range of tiles, walked in groups of 4
+// tile-rows (1-2% faster than 8 on the block's shapes), so tiles that share
+// operand panels share an L2.
 //
 // Determinism: every output element is the sum over ascending 16-wide K
 // steps, one MFMA each, in the same sequence whatever M, BM, the row maps
@@ -72,7 +73,7 @@ constexpr int SLOTS = BK / 8;              // 16-byte slots per row
 constexpr int RPL = 1024 / ROWB;           // rows filled by one 1 KiB wave load
 constexpr int NS = 2;                      // LDS pipeline stages
 constexpr int B_BYTES = BN * BK * 2;       // B bytes per stage
-constexpr int GROUP_M = 8;
+constexpr int GROUP_M = 4;
 constexpr int NWAVES = 8;                  // 2 x 4 waves, two per SIMD
 constexpr int WN = BN * 2 / NWAVES;        // output columns per wave
 // slot swizzle of a 128-byte row (two rows share a 256-byte bank line)
