@@ -66,6 +66,28 @@ def test_dual_chunked_runs_are_bit_identical(name):
         assert torch.equal(out, base), (name, chunk)
 
 
+@pytest.mark.parametrize("name", sorted(DUAL))
+def test_dual_pipelined_chunks_are_bit_identical(name):
+    """The two-stream chunked driver picks each row's modulation by its sequence
+    position like the one-stream one, for chunks that end just before, at and
+    just after the text tokens."""
+    s = DUAL[name]
+    dev = _device(name)
+    base, _, _ = dev.run(0)
+    aux = torch.cuda.Stream()
+    T = s.text_len
+    for chunk in sorted({T - 1, T, T + 1, 100}):
+        if chunk <= 0 or chunk >= s.seq_len:
+            continue
+        plan = X.xema_workspace_layout(dev.cfg, dev.req, chunk)
+        ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+        out = torch.empty_like(base)
+        X.xema_dit_block_fwd_pipelined(dev.cfg, dev.req, dev.x, dev.weights, dev.cond, s.batch, chunk, ws,
+                                       ws.numel(), out, None, aux)
+        torch.cuda.synchronize()
+        assert torch.equal(out, base), (name, chunk)
+
+
 def test_dual_modulation_slot_holds_both_maps():
     s = DUAL["d64_b2"]
     dev = _device("d64_b2")
