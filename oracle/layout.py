@@ -116,7 +116,7 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
     SEQ_PAD tokens.  In a chunked call the attention buffer stays live
     through the chunk's MLP (steps 5-9), so the next chunk's attention may
     run meanwhile on a second stream.  A dual-stream block (reading R24) keeps both modulation
-    vectors, so its mod slot doubles.  At head_dim 64 the QKV projection writes
+    vectors, so its mod slot doubles.  At head_dim 64 and 128 the QKV projection writes
     Q, K and V^T itself (reading R28), so the [tokens, 3D] qkv slot is empty."""
     B, D, F = batch, hidden, mlp_hidden
     c = seq_len if chunk <= 0 or chunk >= seq_len else chunk
@@ -128,7 +128,7 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
         ("k", 2 * B * D * lp, 1, 10),
         ("vt", 2 * B * D * lp, 1, 10),
         ("ln1", 2 * B * c * D, 1, 3),
-        ("qkv", 0 if head_dim == 64 else 6 * B * c * D, 2, 4),
+        ("qkv", 0 if head_dim in (64, 128) else 6 * B * c * D, 2, 4),
         ("wo16", 2 * D * D, 4, 10),
         ("wup16", 2 * F * D, 4, 10),
         ("wdown16", 2 * D * F, 4, 10),

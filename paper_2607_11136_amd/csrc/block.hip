@@ -8,7 +8,7 @@
 //            table, once per call
 //   phase A  for each chunk of c tokens: LN1 (a1) -> QKV GEMM (a2) ->
 //            QK-RMSNorm + RoPE scatter (a3), filling Q, K, V^T for all tokens
-//            (a2 and a3 are one kernel at head_dim 64)
+//            (a2 and a3 are one kernel)
 //   step 4   fp16 copies of W_o, W_up, W_down
 //   phase B  for each chunk of c queries: attention over all keys (a4) ->
 //            out-projection + gated residual (a5) -> LN2 (a6) -> MLP up +
@@ -259,11 +259,12 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
                           mod + txt_delta, s));
   XEMA_TRY(launch_rope_table(geom, c.rope_theta, rope, s));
 
-  // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk.  At head
-  // dim 64 the QKV GEMM's epilogue does the scatter itself (one head per
-  // wave), the qkv slot stays unused and the padding tokens are zeroed once.
-  const bool fused_heads = c.head_dim == 64;
-  // the qkv slot is sized for the unfused path only (empty at head_dim 64)
+  // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk.  The QKV
+  // GEMM's epilogue does the scatter itself (a head per wave at head dim 64,
+  // per two waves at 128), the qkv slot stays unused and the padding tokens
+  // are zeroed once.
+  const bool fused_heads = c.head_dim == 64 || c.head_dim == 128;
+  // the qkv slot is sized for the unfused path only (empty when fused)
   if (!fused_heads && plan.slot_bytes[XEMA_SLOT_QKV] < 6 * B * std::min(ch, L) * D)
     return XEMA_ERR_INVALID_ARG;
   for (int64_t t0 = 0; t0 < L; t0 += ch) {
@@ -274,7 +275,8 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     const QkRopeArgs qa = qk_args(c, r, qkv, (int)t0, (int)cc, w.q_gamma, w.k_gamma, rope, Q, Kk, VT);
     GemmParams g{};
     g.dtype = XEMA_BF16; g.a = ln1; g.b = w.qkv_w; g.M = B * cc; g.N = (int)(3 * D); g.K = (int)D;
-    g.bias = (const uint16_t*)w.qkv_b; g.epilogue = fused_heads ? EPI_QKV_HEADS : XEMA_EPI_BIAS;
+    g.bias = (const uint16_t*)w.qkv_b; g.epilogue =
+        !fused_heads ? XEMA_EPI_BIAS : c.head_dim == 64 ? EPI_QKV_HEADS : EPI_QKV_HEADS_128;
     g.c = qkv; g.c_dtype = XEMA_F16; g.c_map = RowMap{cc, cc, 0}; g.ldc = 3 * D;
     g.qk = qa;
     XEMA_TRY(launch_gemm(g, s));

@@ -173,28 +173,43 @@ __device__ __forceinline__ float pair_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Epilogue of the QKV GEMM at head_dim 64 (EPI_QKV_HEADS): steps a2 and a3
-// fused.  256 divides D, so a tile's columns lie in one section (Q, K or V),
-// and a wave's 64 columns are one head.  Lane (r32, hi) holds, for each of
-// its rows, the head dims 32 j + 8 q + 4 hi + e (j < 2, q < 4, e < 4): half
-// of the head, the other half being in lane r32 + 32 (1 - hi).  Q and K:
-// v = acc + bias, RMS over the 64 dims, times gamma, the 3D RoPE rotation of
-// the pairs (2p, 2p+1) and, for Q, the softmax factor log2(e)/sqrt(d), then
-// one fp16 rounding; stored to [B, H, Lp, 64].  V: rounded to fp16 and
-// transposed through LDS into [B, H, 64, Lp], 8 tokens per 16-byte store.
+// LDS bytes the QKV epilogue uses on a BM-row tile at head_dim HD: the
+// [BM] int4 token positions, at HD = 128 the [NWAVES][BM/2] partial sums of
+// squares, and the [BM][HD/2 + 2] float2 (cos, sin) rows.
+constexpr int qkv_epi_lds_bytes(int BM, int HD) {
+  return BM * 16 + (HD == 128 ? NWAVES * (BM / 2) * 4 : 0) + BM * (HD / 2 + 2) * 8;
+}
+
+// Epilogue of the QKV GEMM (EPI_QKV_HEADS at head_dim 64, EPI_QKV_HEADS_128
+// at 128): steps a2 and a3 fused.  256 divides D, so a tile's columns lie in
+// one section (Q, K or V).  A wave's 64 columns are one head at HD = 64, and
+// one half of a head at HD = 128 (dims 64 * half .., half = wn % 2; the other
+// half is in wave wn ^ 1 of the same rows).  Lane (r32, hi) holds, for each
+// of its rows, the wave's columns 32 j + 8 q + 4 hi + e (j < 2, q < 4,
+// e < 4), the rest being in lane r32 + 32 (1 - hi).  Q and K: v = acc + bias,
+// RMS over the HD dims (at HD = 128 the two waves of a head exchange their
+// partial sums of squares through LDS and add them in the same order, so
+// both scale by the same factor), times gamma, the 3D RoPE rotation of the
+// pairs (2p, 2p+1) and, for Q, the softmax factor log2(e)/sqrt(d), then one
+// fp16 rounding; stored to [B, H, Lp, HD].  V: rounded to fp16 and
+// transposed through LDS into [B, H, HD, Lp], 8 tokens per 16-byte store.
 // Rows are the tokens tok_begin + (m mod rows_per_batch) of batch row
 // m / rows_per_batch; nothing is written for m >= m_end.
-template <int MI, int NJ, int BM>
+template <int MI, int NJ, int BM, int HD>
 __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f32x16 (&acc)[MI][NJ],
                                                    int64_t m0, int64_t m_end, int n0, int wm, int wn,
                                                    int lane, int wave, uint8_t* smem,
                                                    const uint16_t* __restrict__ bias) {
-  static_assert(NJ == 2, "one 64-dim head per wave");
+  static_assert(NJ == 2, "64 columns per wave");
+  static_assert(HD == 64 || HD == 128, "head dims");
+  constexpr int HALVES = HD / 64;   // waves per head
+  constexpr int NP = HD / 2;        // rotated pairs per head
   const QkRopeArgs& a = p.qk;
   const int r32 = lane & 31, hi = lane >> 5;
-  const int D = a.heads * 64;
+  const int D = a.heads * HD;
   const int sect = n0 / D;
-  const int h = (n0 - sect * D) / 64 + wn;
+  const int h = (n0 - sect * D) / HD + wn / HALVES;
+  const int half = wn % HALVES;
   const int64_t rpb = p.c_map.rows_per_batch;
   const int64_t Lp = a.padded_len;
   const int col0 = n0 + wn * 64 + 4 * hi;
@@ -210,17 +225,21 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) load4f<uint16_t>(gam + 4 * hi + j * 32 + 8 * q, g[j][q]);
+      for (int q = 0; q < 4; ++q) load4f<uint16_t>(gam + half * 64 + 4 * hi + j * 32 + 8 * q, g[j][q]);
     const float f = sect == 0 ? a.q_scale : 1.0f;
     f16* dst = sect == 0 ? a.q : a.k;
-    // (cos, sin) of the tile's BM tokens x 32 pairs, shared by its four heads:
-    // [BM][32] float2 rows padded to 272 bytes (conflict-free 16-byte reads
-    // by 16 consecutive rows), after [BM] int4 (valid, t, y, w) per token.
-    // Pair p of a head rotates on axis 0, 1 or 2 when it falls in that
-    // axis' range of the cumulative dims/2 (table: axis-major, then position).
-    constexpr int CS_STRIDE = 34;  // float2 per padded row
+    // (cos, sin) of the tile's BM tokens x NP pairs, shared by its heads:
+    // [BM][NP] float2 rows padded by 16 bytes (conflict-free 16-byte reads by
+    // 16 consecutive rows), after [BM] int4 (valid, t, y, w) per token and,
+    // at HD = 128, the partial sums of squares.  Pair p of a head rotates on
+    // axis 0, 1 or 2 when it falls in that axis' range of the cumulative
+    // dims/2 (table: axis-major, then position).
+    constexpr int CS_STRIDE = NP + 2;  // float2 per padded row
+    constexpr int SS_BYTES = HALVES > 1 ? NWAVES * (BM / 2) * 4 : 0;
+    static_assert(qkv_epi_lds_bytes(BM, HD) == BM * 16 + SS_BYTES + BM * CS_STRIDE * 8, "LDS plan");
     int4* pos_lds = reinterpret_cast<int4*>(smem);
-    float2* cs_lds = reinterpret_cast<float2*>(smem + BM * 16);
+    float* ss_lds = reinterpret_cast<float*>(smem + BM * 16);
+    float2* cs_lds = reinterpret_cast<float2*>(smem + BM * 16 + SS_BYTES);
     __syncthreads();  // every wave is done reading the operand stages
     {
       const int gw = max(a.geom.grid[2], 1), hw = max(a.geom.grid[1] * a.geom.grid[2], 1);
@@ -238,14 +257,32 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
     {
       const int np0 = a.geom.dims[0] / 2, np1 = a.geom.dims[1] / 2, np2 = a.geom.dims[2] / 2;
       const int tb1 = a.geom.grid[0] * np0, tb2 = tb1 + a.geom.grid[1] * np1;
-      for (int e = (int)threadIdx.x; e < BM * 32; e += NWAVES * 64) {
-        const int t = e >> 5, pr = e & 31;
+      for (int e = (int)threadIdx.x; e < BM * NP; e += NWAVES * 64) {
+        const int t = e / NP, pr = e % NP;
         const int4 ps = pos_lds[t];
         int idx = -1;
         if (pr < np0) idx = ps.y * np0 + pr;
         else if (pr < np0 + np1) idx = tb1 + ps.z * np1 + (pr - np0);
         else if (pr < np0 + np1 + np2) idx = tb2 + ps.w * np2 + (pr - np0 - np1);
         cs_lds[t * CS_STRIDE + pr] = (ps.x && idx >= 0) ? a.table[idx] : make_float2(1.f, 0.f);
+      }
+    }
+    if constexpr (HALVES > 1) {
+      // this wave's sum of squares over its 64 dims, per row
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        float ss = 0.f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float v = acc[i][j][4 * q + e] + bv[j][q][e];
+              ss = fmaf(v, v, ss);
+            }
+        ss = pair_sum(ss);
+        if (hi == 0) ss_lds[wave * (BM / 2) + i * 32 + r32] = ss;
       }
     }
     __syncthreads();
@@ -266,11 +303,17 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
             v[j][q][e] = acc[i][j][4 * q + e] + bv[j][q][e];
             ss = fmaf(v[j][q][e], v[j][q][e], ss);
           }
-      ss = pair_sum(ss);
+      if constexpr (HALVES > 1) {
+        // dims 0..63 (wave wave - half) plus dims 64..127, in that order
+        const float* sp = ss_lds + (wave - half) * (BM / 2) + i * 32 + r32;
+        ss = sp[0] + sp[BM / 2];
+      } else {
+        ss = pair_sum(ss);
+      }
       // 1/sqrt(mean + eps) with the hardware reciprocal square root (1 ulp)
-      const float r = __builtin_amdgcn_rsqf(ss * (1.0f / 64.0f) + a.qk_eps);
-      const float2* csr = cs_lds + (wm * (BM / 2) + i * 32 + r32) * CS_STRIDE + 2 * hi;
-      f16* row = dst + (((int64_t)bb * a.heads + h) * Lp + tok) * 64;
+      const float r = __builtin_amdgcn_rsqf(ss * (1.0f / (float)HD) + a.qk_eps);
+      const float2* csr = cs_lds + (wm * (BM / 2) + i * 32 + r32) * CS_STRIDE + half * 32 + 2 * hi;
+      f16* row = dst + (((int64_t)bb * a.heads + h) * Lp + tok) * HD + half * 64;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         f16x4 o[4];
@@ -317,7 +360,7 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
     const f16x8 vals = *reinterpret_cast<const f16x8*>(lds + d * TPW + g8 * 8);
     const int64_t bb = mf / rpb, ii = mf - bb * rpb;
     const int tok = a.tok_begin + (int)ii;
-    f16* vrow = a.vt + (((int64_t)bb * a.heads + h) * 64 + d) * Lp;
+    f16* vrow = a.vt + (((int64_t)bb * a.heads + h) * HD + half * 64 + d) * Lp;
     if (mf + 8 <= m_end && ii + 8 <= rpb && (tok & 7) == 0) {
       *reinterpret_cast<f16x8*>(vrow + tok) = vals;
     } else {
@@ -326,7 +369,8 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
         const int64_t m = mf + e;
         if (m < m_end) {
           const int64_t b2 = m / rpb;
-          a.vt[(((int64_t)b2 * a.heads + h) * 64 + d) * Lp + a.tok_begin + (m - b2 * rpb)] = vals[e];
+          a.vt[(((int64_t)b2 * a.heads + h) * HD + half * 64 + d) * Lp + a.tok_begin + (m - b2 * rpb)] =
+              vals[e];
         }
       }
     }
@@ -507,8 +551,9 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
   // before the workgroup can end
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 
-  if constexpr (EPI == EPI_QKV_HEADS) {
-    epilogue_qkv_heads<MI, NJ, BM>(p, acc, m0, m_end, n0, wm, wn, lane, wave, smem_raw, bias);
+  if constexpr (EPI == EPI_QKV_HEADS || EPI == EPI_QKV_HEADS_128) {
+    epilogue_qkv_heads<MI, NJ, BM, EPI == EPI_QKV_HEADS ? 64 : 128>(p, acc, m0, m_end, n0, wm, wn, lane,
+                                                                   wave, smem_raw, bias);
     return;
   }
 
@@ -609,7 +654,10 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t s
                                                          CT* __restrict__ cout,
                                                          const RT* __restrict__ resid,
                                                          const float* __restrict__ gate) {
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[NS * (256 * BK * 2 + B_BYTES)];
+  // the operand stages; the QKV epilogue at head_dim 128 needs a little more
+  constexpr int STAGES = NS * (256 * BK * 2 + B_BYTES);
+  constexpr int EPI_LDS = EPI == EPI_QKV_HEADS_128 ? qkv_epi_lds_bytes(256, 128) : 0;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES > EPI_LDS ? STAGES : EPI_LDS];
   if ((int)blockIdx.x < tiles_big)
     gemm_tile<T, EPI, CT, RT, 256>(p, 0, split, (int)blockIdx.x, smem, bias, cout, resid, gate);
   else
@@ -699,6 +747,9 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
     case EPI_QKV_HEADS:
       if (h) return hipErrorInvalidValue;
       return launch_t<bf16, EPI_QKV_HEADS, f16, float>(p, s);
+    case EPI_QKV_HEADS_128:
+      if (h) return hipErrorInvalidValue;
+      return launch_t<bf16, EPI_QKV_HEADS_128, f16, float>(p, s);
     default:
       return hipErrorInvalidValue;
   }

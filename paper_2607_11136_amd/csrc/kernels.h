@@ -62,10 +62,12 @@ struct GemmParams {
   QkRopeArgs qk;    // EPI_QKV_HEADS: rows are tokens [qk.tok_begin, +c_map.rows_per_batch)
 };
 
-// Internal epilogue of the QKV GEMM at head_dim 64 (steps a2 + a3 in one
-// kernel): bias, QK-RMSNorm, 3D RoPE and the scatter into Q, K and V^T,
-// without the [tokens, 3D] intermediate.  Not accepted by xema_op_gemm.
+// Internal epilogues of the QKV GEMM (steps a2 + a3 in one kernel): bias,
+// QK-RMSNorm, 3D RoPE and the scatter into Q, K and V^T, without the
+// [tokens, 3D] intermediate, at head_dim 64 and 128.  Not accepted by
+// xema_op_gemm.
 constexpr int EPI_QKV_HEADS = 3;
+constexpr int EPI_QKV_HEADS_128 = 4;
 
 struct AttnParams {
   const _Float16* q;

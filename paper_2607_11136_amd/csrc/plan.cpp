@@ -125,7 +125,7 @@ int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t
       {2 * B * D * lp, 1, 10},                     // XEMA_SLOT_K
       {2 * B * D * lp, 1, 10},                     // XEMA_SLOT_VT
       {2 * B * c * D, 1, 3},                       // XEMA_SLOT_LN1
-      {cfg.head_dim == 64 ? 0 : 6 * B * c * D, 2, 4},  // XEMA_SLOT_QKV (unused at d = 64)
+      {cfg.head_dim == 64 || cfg.head_dim == 128 ? 0 : 6 * B * c * D, 2, 4},  // XEMA_SLOT_QKV (unused when fused)
       {2 * D * D, 4, 10},                          // XEMA_SLOT_WO16
       {2 * F * D, 4, 10},                          // XEMA_SLOT_WUP16
       {2 * D * F, 4, 10},                          // XEMA_SLOT_WDOWN16
