@@ -121,8 +121,8 @@ enum {
   XEMA_SLOT_K,         /* fp16 [B, H, Lp, d]                 life [1, 10) */
   XEMA_SLOT_VT,        /* fp16 [B, H, d, Lp] (transposed)    life [1, 10) */
   XEMA_SLOT_LN1,       /* bf16 [B*c, D]                      life [1, 3)  */
-  XEMA_SLOT_QKV,       /* fp16 [B*c, 3D]  life [2, 4); empty at head_dim 64, where the
-                          QKV GEMM writes Q, K and V^T itself */
+  XEMA_SLOT_QKV,       /* fp16 [B*c, 3D]  life [2, 4); empty at head_dim 64 and 128,
+                          where the QKV GEMM writes Q, K and V^T itself */
   XEMA_SLOT_WO16,      /* fp16 [D, D]                        life [4, 10) */
   XEMA_SLOT_WUP16,     /* fp16 [F, D]                        life [4, 10) */
   XEMA_SLOT_WDOWN16,   /* fp16 [D, F]                        life [4, 10) */
