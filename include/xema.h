@@ -21,6 +21,32 @@
  *     device state.  All functions are thread-safe.
  *   - Device pointers must be 16-byte aligned; the workspace 256-byte aligned.
  *   - Token/weight/conditioning inputs are bfloat16 (bit patterns, uint16).
+ *
+ * Precision contract (where this library departs from a bf16-everywhere
+ * block, and why).  The block output `out` and the residual stream x1 are
+ * fp32: one bf16 rounding of the output alone costs a mean absolute error of
+ * about 2e-3 on unit-variance activations, the whole accuracy bar of the
+ * path, so the output is handed over unrounded and a caller that stores bf16
+ * rounds once itself.  The contractions of attention, the output projection
+ * and the MLP run fp16 MFMA (fp32 accumulation): V, the attention
+ * probabilities P, the attention output O, the LN2 output h2, the MLP hidden
+ * activations g and the fp16 copies of W_o, W_up and W_down are fp16, which
+ * has three more mantissa bits than bf16 and the same MFMA rate on gfx950,
+ * but a range of +-65504.  The QKV projection is bf16 MFMA on the bf16 LN1
+ * output and the caller's bf16 W_qkv; Q and K are stored fp16 after
+ * QK-RMSNorm, RoPE and the softmax factor.  Range limits:
+ *   - V, h2 and g must stay below 65504 in magnitude (they round to inf
+ *     at 65520 and above); O is a convex combination of V rows and cannot
+ *     leave the range when V does not;
+ *   - Q and K are bounded by sqrt(d) |gamma| after the RMS normalisation;
+ *   - weights converted to fp16 must be below 65504 in magnitude, and lose
+ *     relative precision below 2^-14 (fp16 subnormals) and vanish below
+ *     2^-25.
+ * Every fp16 store of V, Q, K, h2 and g and every converted weight is
+ * checked: a value at or beyond the fp16 range (or NaN) sets a flag in the
+ * arena's status slot, which xema_block_status reads after the call.  A
+ * call whose status is not clean has produced non-finite or saturated
+ * intermediates and its output must not be used.
  */
 #ifndef XEMA_H_
 #define XEMA_H_
@@ -40,8 +66,19 @@ typedef enum {
   XEMA_ERR_BUDGET_TOO_SMALL = -3,     /* even the smallest chunk exceeds the budget */
   XEMA_ERR_WORKSPACE_TOO_SMALL = -4,  /* workspace_bytes below the plan's arena size */
   XEMA_ERR_MISALIGNED = -5,           /* pointer alignment violated */
-  XEMA_ERR_HIP = -6                   /* a HIP launch or runtime call failed */
+  XEMA_ERR_HIP = -6,                  /* a HIP launch or runtime call failed */
+  XEMA_ERR_RANGE = -7                 /* an fp16 intermediate left its range (xema_block_status) */
 } xema_status;
+
+/* Bits of the range status (xema_block_status): which fp16 intermediate
+ * held a value at or beyond +-65520 (rounds to inf) or a NaN.             */
+enum {
+  XEMA_RANGE_QKV = 1,       /* Q, K or V written by the QKV projection's epilogue */
+  XEMA_RANGE_LN2 = 2,       /* h2, the LN2 + modulation output */
+  XEMA_RANGE_MLP = 4,       /* g, the MLP hidden activations after GELU */
+  XEMA_RANGE_WEIGHTS = 8    /* a phase-B weight converted to fp16 in the call */
+};
+#define XEMA_STATUS_WORDS 4
 
 #define XEMA_MAX_SLOTS 16
 #define XEMA_CHUNK_GRANULE 256        /* planned chunks are multiples of this, or all */
@@ -62,12 +99,19 @@ typedef enum {
  *               2: dual-stream block, whose text tokens take their shift,
  *               scale and gate from a second AdaLN map of their own
  *               (xema_block_weights.ada_txt_w / ada_txt_b), the visual
- *               tokens from ada_w / ada_b; every other weight is shared   */
+ *               tokens from ada_w / ada_b; every other weight is shared
+ *   weights_f16 0: o_w, up_w and down_w are bf16 like every other weight and
+ *               each call converts them into fp16 arena slots;
+ *               1: the caller passes o_w, up_w and down_w already in fp16
+ *               (converted once per model, e.g. with xema_op_convert_f16),
+ *               which the block reads directly (no conversion, no arena
+ *               slots for the copies; bit-identical output)              */
 typedef struct {
   int32_t hidden, heads, head_dim, mlp_hidden, cond_dim;
   int32_t rope_dims[3];
   float rope_theta, ln_eps, qk_eps;
   int32_t modulation_streams;
+  int32_t weights_f16;
 } xema_block_cfg;
 
 /* One batched call: `batch` requests of one template (the paper batches only
@@ -87,6 +131,8 @@ typedef struct {
  *   o_w [D, D]       o_b [D]        attention output projection
  *   up_w [F, D]      up_b [F]       MLP up projection (GELU-tanh follows)
  *   down_w [D, F]    down_b [D]     MLP down projection
+ *                                   (o_w, up_w, down_w are fp16 instead
+ *                                   when xema_block_cfg.weights_f16 = 1)
  *   ada_txt_w [6D, D_c]  ada_txt_b [6D]  the text tokens' AdaLN map of a
  *                                   dual-stream block (modulation_streams = 2),
  *                                   rows ordered as ada_w; ignored otherwise */
@@ -113,7 +159,10 @@ typedef struct {
 /* Slot ids of xema_plan.  Steps: 0 AdaLN map + RoPE table; phase A (per token
  * chunk) 1 LN1, 2 QKV projection, 3 QK-norm/RoPE scatter; 4 fp16 copies of the
  * phase-B weights; phase B (per query chunk) 5 attention, 6 out-projection +
- * gated residual, 7 LN2, 8 MLP up + GELU, 9 MLP down + gated residual.     */
+ * gated residual, 7 LN2, 8 MLP up + GELU, 9 MLP down + gated residual.
+ * The qkv slot is empty: head_dim is 64 or 128, where the QKV GEMM's
+ * epilogue writes Q, K and V^T itself; the three weight-copy slots are
+ * empty when cfg.weights_f16 = 1.                                          */
 enum {
   XEMA_SLOT_MOD = 0,   /* fp32 [S, B, 6D], S modulation streams (visual first) life [0, 10) */
   XEMA_SLOT_ROPE,      /* fp32 cos/sin per axis position     life [0, 4)  */
@@ -131,6 +180,8 @@ enum {
   XEMA_SLOT_X1,        /* fp32 [B*c, D]                      life [6, 10) */
   XEMA_SLOT_LN2,       /* fp16 [B*c, D]                      life [7, 9)  */
   XEMA_SLOT_HID,       /* fp16 [B*c, F]                      life [8, 10) */
+  XEMA_SLOT_STATUS,    /* uint32 [XEMA_STATUS_WORDS] range flags, cleared at
+                          step 0                             life [0, 10) */
   XEMA_NUM_SLOTS
 };
 
@@ -178,8 +229,9 @@ XEMA_API int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request* 
  *            xema_workspace_bytes(cfg, req, chunk_tokens) bytes, 256-byte
  *            aligned, owned by the caller.  Its contents on entry are ignored;
  *            on return it holds the intermediates at the layout's offsets.
- *   out      device, fp32 [B, L, D], written once per element; must not
- *            overlap tokens, weights, cond or the workspace.
+ *   out      device, fp32 [B, L, D] (fp32, not bf16: see the precision
+ *            contract above), written once per element; must not overlap
+ *            tokens, weights, cond or the workspace.
  * Computes, per batch element (the block definition: AdaLN-modulated
  * LayerNorm, QKV projection, QK-RMSNorm, 3D RoPE, joint full self-attention,
  * gated output projection, LayerNorm, GELU-tanh MLP, gated residual):
@@ -248,6 +300,16 @@ XEMA_API int xema_dit_block_fwd_pipelined(const xema_block_cfg* cfg, const xema_
                                  const void* cond, int32_t batch_group, int32_t chunk_tokens,
                                  void* workspace, int64_t workspace_bytes,
                                  void* out, void* stream, void* aux_stream);
+
+/* Range status of the last block call that used this workspace with this
+ * layout (any xema_dit_block_fwd* entry point): waits for `stream`, copies
+ * the status slot to the host and sets *flags to the XEMA_RANGE_* bits of
+ * the fp16 intermediates that left their range (0: none).  Returns XEMA_OK
+ * when *flags is 0 and XEMA_ERR_RANGE otherwise; XEMA_ERR_INVALID_ARG for
+ * NULL pointers or a layout without a status slot; XEMA_ERR_HIP if the copy
+ * fails.  Synchronous; allocates nothing.                                 */
+XEMA_API int xema_block_status(const xema_plan* plan, const void* workspace, void* stream,
+                               uint32_t* flags);
 
 /* Static string naming a status code. */
 XEMA_API const char* xema_status_str(int status);

@@ -50,16 +50,19 @@ def adaln_modulation(cond: np.ndarray, w_ada: np.ndarray, b_ada: np.ndarray) -> 
     return cond @ w_ada.T + b_ada
 
 
-def row_modulation(cond: np.ndarray, w: Dict[str, np.ndarray], text_len: int, L: int) -> np.ndarray:
-    """The modulation vector of every token: [B, L, 6D].  One AdaLN map for
-    all tokens (reading R1), or with a second map for the text tokens
-    (reading R24): rows below text_len take m_txt, the rest m."""
+def row_modulation(cond: np.ndarray, w: Dict[str, np.ndarray], text_len: int, L: int,
+                   rows: Optional[Sequence[int]] = None) -> np.ndarray:
+    """The modulation vector of every token, or of the sequence positions in
+    `rows`: [B, L or len(rows), 6D].  One AdaLN map for all tokens (reading
+    R1), or with a second map for the text tokens (reading R24): positions
+    below text_len take m_txt, the rest m."""
+    sel = np.arange(L) if rows is None else np.asarray(rows, dtype=np.int64)
     m = adaln_modulation(cond, w["ada_w"], w["ada_b"])
-    rows = np.repeat(m[:, None, :], L, axis=1)
+    out = np.repeat(m[:, None, :], sel.size, axis=1)
     if "ada_txt_w" in w:
         m_txt = adaln_modulation(cond, w["ada_txt_w"], w["ada_txt_b"])
-        rows[:, :text_len, :] = m_txt[:, None, :]
-    return rows
+        out[:, sel < text_len, :] = m_txt[:, None, :]
+    return out
 
 
 def split_modulation(m: np.ndarray) -> Tuple[np.ndarray, ...]:
@@ -204,6 +207,53 @@ def qkv_heads(h: np.ndarray, w: Dict[str, np.ndarray], heads: int, head_dim: int
     return rope_rotate(q, ang), rope_rotate(k, ang), v
 
 
+def block_prepare(x: np.ndarray, cond: np.ndarray, w: Dict[str, np.ndarray], *,
+                  heads: int, head_dim: int, text_len: int, grid: Tuple[int, int, int],
+                  rope_dims: Sequence[int], rope_theta: float = 10000.0,
+                  ln_eps: float = 1e-6, qk_eps: float = 1e-6,
+                  coords: Optional[np.ndarray] = None) -> dict:
+    """Steps 1-5 for every token of every sequence: the normalised and rotated
+    q, k and the v of each batch element, which every output row needs (a
+    query attends to all L keys).  Returns a dict that block_rows consumes."""
+    B, L, D = x.shape
+    if coords is None:
+        coords = token_coords(text_len, grid)
+    assert coords.shape[0] == L and heads * head_dim == D
+    qkv = []
+    for b in range(B):
+        # the modulation vectors of 8192 rows at a time (LayerNorm is per row,
+        # so the row blocks only bound memory)
+        h = np.empty((L, D), dtype=np.float64)
+        for r0 in range(0, L, 8192):
+            sel = np.arange(r0, min(L, r0 + 8192))
+            m = row_modulation(cond[b:b + 1], w, text_len, L, rows=sel)[0]
+            h[sel] = modulate(layer_norm(x[b, sel], ln_eps), m[:, 0:D], m[:, D:2 * D])
+        qkv.append(qkv_heads(h, w, heads, head_dim, coords, rope_dims, rope_theta, qk_eps))
+    return {"x": x, "cond": cond, "w": w, "qkv": qkv, "heads": heads, "head_dim": head_dim,
+            "text_len": text_len, "ln_eps": ln_eps}
+
+
+def block_rows(prep: dict, rows: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Steps 6-10 for the sequence positions in `rows` (all when None) of
+    every batch element: [B, len(rows), D]."""
+    x, w, heads, head_dim = prep["x"], prep["w"], prep["heads"], prep["head_dim"]
+    B, L, D = x.shape
+    sel = np.arange(L) if rows is None else np.asarray(rows, dtype=np.int64)
+    _, _, gate1, shift2, scale2, gate2 = split_modulation(
+        row_modulation(prep["cond"], w, prep["text_len"], L, rows=sel))  # each [B, R, D]
+    out = np.empty((B, sel.size, D), dtype=np.float64)
+    for b in range(B):
+        q, k, v = prep["qkv"][b]
+        o = np.empty((sel.size, heads, head_dim), dtype=np.float64)
+        for j in range(heads):
+            o[:, j, :] = attention(q[sel, j, :], k[:, j, :], v[:, j, :])
+        x1 = x[b][sel] + gate1[b] * linear(o.reshape(sel.size, D), w["o_w"], w["o_b"])
+        h2 = modulate(layer_norm(x1, prep["ln_eps"]), shift2[b], scale2[b])
+        g = gelu_tanh(linear(h2, w["up_w"], w["up_b"]))
+        out[b] = x1 + gate2[b] * linear(g, w["down_w"], w["down_b"])
+    return out
+
+
 def block_forward(x: np.ndarray, cond: np.ndarray, w: Dict[str, np.ndarray], *,
                   heads: int, head_dim: int, text_len: int, grid: Tuple[int, int, int],
                   rope_dims: Sequence[int], rope_theta: float = 10000.0,
@@ -217,32 +267,21 @@ def block_forward(x: np.ndarray, cond: np.ndarray, w: Dict[str, np.ndarray], *,
     [B, L, D], or [B, len(rows), D] when `rows` selects output rows (keys and
     values are still formed from every token).  `coords` overrides the token
     grid coordinates (used only by tests that move the grid)."""
-    B, L, D = x.shape
-    if coords is None:
-        coords = token_coords(text_len, grid)
-    assert coords.shape[0] == L and heads * head_dim == D
-    sel = np.arange(L) if rows is None else np.asarray(rows, dtype=np.int64)
-    shift1, scale1, gate1, shift2, scale2, gate2 = split_modulation(
-        row_modulation(cond, w, text_len, L))  # each [B, L, D]
-    out = np.empty((B, sel.size, D), dtype=np.float64)
-    for b in range(B):
-        xb = x[b]
-        h = modulate(layer_norm(xb, ln_eps), shift1[b], scale1[b])
-        q, k, v = qkv_heads(h, w, heads, head_dim, coords, rope_dims, rope_theta, qk_eps)
-        o = np.empty((sel.size, heads, head_dim), dtype=np.float64)
-        for j in range(heads):
-            o[:, j, :] = attention(q[sel, j, :], k[:, j, :], v[:, j, :])
-        x1 = xb[sel] + gate1[b][sel] * linear(o.reshape(sel.size, D), w["o_w"], w["o_b"])
-        h2 = modulate(layer_norm(x1, ln_eps), shift2[b][sel], scale2[b][sel])
-        g = gelu_tanh(linear(h2, w["up_w"], w["up_b"]))
-        out[b] = x1 + gate2[b][sel] * linear(g, w["down_w"], w["down_b"])
-    return out
+    prep = block_prepare(x, cond, w, heads=heads, head_dim=head_dim, text_len=text_len, grid=grid,
+                         rope_dims=rope_dims, rope_theta=rope_theta, ln_eps=ln_eps, qk_eps=qk_eps,
+                         coords=coords)
+    return block_rows(prep, rows)
+
+
+def prepare_shape(inputs) -> dict:
+    """block_prepare on a workloads.Inputs bundle (bf16 values upcast exactly)."""
+    s = inputs.shape
+    return block_prepare(inputs.f64("x"), inputs.f64("cond"), inputs.weights_f64(),
+                         heads=s.heads, head_dim=s.head_dim, text_len=s.text_len,
+                         grid=s.grid, rope_dims=s.rope_dims, rope_theta=s.rope_theta,
+                         ln_eps=s.ln_eps, qk_eps=s.qk_eps)
 
 
 def block_forward_shape(inputs, rows=None) -> np.ndarray:
     """block_forward on a workloads.Inputs bundle (bf16 values upcast exactly)."""
-    s = inputs.shape
-    return block_forward(inputs.f64("x"), inputs.f64("cond"), inputs.weights_f64(),
-                         heads=s.heads, head_dim=s.head_dim, text_len=s.text_len,
-                         grid=s.grid, rope_dims=s.rope_dims, rope_theta=s.rope_theta,
-                         ln_eps=s.ln_eps, qk_eps=s.qk_eps, rows=rows)
+    return block_rows(prepare_shape(inputs), rows)

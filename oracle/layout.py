@@ -33,7 +33,8 @@ GRANULE = 256          # candidate chunk sizes are multiples of this, or "all"
 SEQ_PAD = 128          # per-head sequence storage is padded to this many tokens
 
 SLOT_NAMES = ("mod", "rope", "q", "k", "vt", "ln1", "qkv", "wo16", "wup16", "wdown16",
-              "attn", "x1", "ln2", "hid")
+              "attn", "x1", "ln2", "hid", "status")
+STATUS_BYTES = 16      # four range-flag words
 
 
 def round_up(x: int, a: int) -> int:
@@ -104,7 +105,7 @@ def rope_table_bytes(grid: Sequence[int], rope_dims: Sequence[int]) -> int:
 
 def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
                   grid: Sequence[int], rope_dims: Sequence[int], chunk: int,
-                  modulation_streams: int = 1, head_dim: int = 0) -> List[Tensor]:
+                  modulation_streams: int = 1, weights_f16: int = 0) -> List[Tensor]:
     """Slot table of one block call with `chunk` tokens per sequence per chunk.
 
     Steps (folded over the chunk loops): 0 = AdaLN map and RoPE table;
@@ -116,8 +117,11 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
     SEQ_PAD tokens.  In a chunked call the attention buffer stays live
     through the chunk's MLP (steps 5-9), so the next chunk's attention may
     run meanwhile on a second stream.  A dual-stream block (reading R24) keeps both modulation
-    vectors, so its mod slot doubles.  At head_dim 64 and 128 the QKV projection writes
-    Q, K and V^T itself (reading R28), so the [tokens, 3D] qkv slot is empty."""
+    vectors, so its mod slot doubles.  The QKV projection writes Q, K and V^T
+    itself (reading R28; head_dim is 64 or 128), so the [tokens, 3D] qkv slot
+    is empty.  With weights_f16 the caller passes W_o, W_up and W_down in
+    fp16 and the three copy slots are empty.  The status slot holds the
+    range flags for the whole call."""
     B, D, F = batch, hidden, mlp_hidden
     c = seq_len if chunk <= 0 or chunk >= seq_len else chunk
     lp = padded_len(seq_len)
@@ -128,14 +132,15 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
         ("k", 2 * B * D * lp, 1, 10),
         ("vt", 2 * B * D * lp, 1, 10),
         ("ln1", 2 * B * c * D, 1, 3),
-        ("qkv", 0 if head_dim in (64, 128) else 6 * B * c * D, 2, 4),
-        ("wo16", 2 * D * D, 4, 10),
-        ("wup16", 2 * F * D, 4, 10),
-        ("wdown16", 2 * D * F, 4, 10),
+        ("qkv", 0, 2, 4),
+        ("wo16", 0 if weights_f16 else 2 * D * D, 4, 10),
+        ("wup16", 0 if weights_f16 else 2 * F * D, 4, 10),
+        ("wdown16", 0 if weights_f16 else 2 * D * F, 4, 10),
         ("attn", 2 * B * c * D, 5, 10 if c < seq_len else 7),
         ("x1", 4 * B * c * D, 6, 10),
         ("ln2", 2 * B * c * D, 7, 9),
         ("hid", 2 * B * c * F, 8, 10),
+        ("status", STATUS_BYTES, 0, 10),
     ]
     assert tuple(n for n, *_ in spec) == SLOT_NAMES
     return [Tensor(i, s, b, e) for i, (_, s, b, e) in enumerate(spec)]
@@ -144,7 +149,8 @@ def block_tensors(batch: int, seq_len: int, hidden: int, mlp_hidden: int,
 def workspace_bytes(shape, chunk: int) -> int:
     """Arena bytes (Algorithm 1 peak) for a workloads.BlockShape and chunk size."""
     ts = block_tensors(shape.batch, shape.seq_len, shape.hidden, shape.mlp_hidden,
-                       shape.grid, shape.rope_dims, chunk, shape.modulation_streams, shape.head_dim)
+                       shape.grid, shape.rope_dims, chunk, shape.modulation_streams,
+                       getattr(shape, "weights_f16", 0))
     return static_layout(ts)[1]
 
 

@@ -23,6 +23,11 @@ XEMA_ERR_BUDGET_TOO_SMALL = -3
 XEMA_ERR_WORKSPACE_TOO_SMALL = -4
 XEMA_ERR_MISALIGNED = -5
 XEMA_ERR_HIP = -6
+XEMA_ERR_RANGE = -7
+
+# range status bits (xema_block_status)
+XEMA_RANGE_QKV, XEMA_RANGE_LN2, XEMA_RANGE_MLP, XEMA_RANGE_WEIGHTS = 1, 2, 4, 8
+XEMA_STATUS_WORDS = 4
 
 XEMA_MAX_SLOTS = 16
 XEMA_CHUNK_GRANULE = 256
@@ -32,7 +37,7 @@ XEMA_BF16, XEMA_F16, XEMA_F32 = 0, 1, 2
 XEMA_EPI_BIAS, XEMA_EPI_BIAS_GELU, XEMA_EPI_GATED_RESIDUAL = 0, 1, 2
 
 SLOT_NAMES = ("mod", "rope", "q", "k", "vt", "ln1", "qkv", "wo16", "wup16", "wdown16",
-              "attn", "x1", "ln2", "hid")
+              "attn", "x1", "ln2", "hid", "status")
 SLOT = {n: i for i, n in enumerate(SLOT_NAMES)}
 
 WEIGHT_FIELDS = ("ada_w", "ada_b", "qkv_w", "qkv_b", "q_gamma", "k_gamma",
@@ -52,7 +57,7 @@ class BlockCfg(ctypes.Structure):
                 ("mlp_hidden", ctypes.c_int32), ("cond_dim", ctypes.c_int32),
                 ("rope_dims", ctypes.c_int32 * 3), ("rope_theta", ctypes.c_float),
                 ("ln_eps", ctypes.c_float), ("qk_eps", ctypes.c_float),
-                ("modulation_streams", ctypes.c_int32)]
+                ("modulation_streams", ctypes.c_int32), ("weights_f16", ctypes.c_int32)]
 
 
 class Request(ctypes.Structure):
@@ -151,6 +156,7 @@ _SIGNATURES = {
     "xema_dit_block_fwd_pipelined": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
                                                     ctypes.POINTER(BlockWeights), _P, _I32, _I32, _P, _I64, _P,
                                                     _P, _P]),
+    "xema_block_status": (ctypes.c_int, [ctypes.POINTER(Plan), _P, _P, ctypes.POINTER(ctypes.c_uint32)]),
     "xema_vae_upconv_weight_bytes": (ctypes.c_int, [_I32, _I32, ctypes.POINTER(_I64)]),
     "xema_vae_upconv_prepare": (ctypes.c_int, [_P, _I32, _I32, _P, _P]),
     "xema_vae_upconv": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _I32, _I32, _I32, _P, _P]),
@@ -204,13 +210,14 @@ def _stream(stream) -> Optional[int]:
 
 def block_cfg(hidden: int, heads: int, head_dim: int, mlp_hidden: int, cond_dim: int,
               rope_dims: Sequence[int], rope_theta: float = 10000.0, ln_eps: float = 1e-6,
-              qk_eps: float = 1e-6, modulation_streams: int = 1) -> BlockCfg:
+              qk_eps: float = 1e-6, modulation_streams: int = 1, weights_f16: int = 0) -> BlockCfg:
     c = BlockCfg()
     c.hidden, c.heads, c.head_dim, c.mlp_hidden, c.cond_dim = hidden, heads, head_dim, mlp_hidden, cond_dim
     for i in range(3):
         c.rope_dims[i] = int(rope_dims[i])
     c.rope_theta, c.ln_eps, c.qk_eps = rope_theta, ln_eps, qk_eps
     c.modulation_streams = modulation_streams
+    c.weights_f16 = weights_f16
     return c
 
 
@@ -288,6 +295,16 @@ def xema_dit_block_fwd(cfg: BlockCfg, req: Request, tokens, weights: BlockWeight
                                     ctypes.byref(weights), _ptr(cond), chunk_tokens,
                                     _ptr(workspace), int(workspace_bytes), _ptr(out),
                                     _stream(stream)), "xema_dit_block_fwd")
+
+
+def xema_block_status(plan: Plan, workspace, stream=None) -> int:
+    """Range flags (XEMA_RANGE_* bits, 0 when clean) of the last block call
+    on this workspace; waits for the stream."""
+    flags = ctypes.c_uint32()
+    st = lib().xema_block_status(ctypes.byref(plan), _ptr(workspace), _stream(stream), ctypes.byref(flags))
+    if st not in (XEMA_OK, XEMA_ERR_RANGE):
+        raise XemaError(st, "xema_block_status")
+    return flags.value
 
 
 def xema_workspace_plan_serial(cfg: BlockCfg, req: Request, budget_bytes: int):

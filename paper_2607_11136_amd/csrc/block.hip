@@ -114,13 +114,14 @@ static int check_gemm(const xema_gemm_args* a) {
 }
 
 static GemmParams to_params(const xema_gemm_args& a) {
-  GemmParams p;
+  GemmParams p{};
   p.dtype = a.dtype; p.a = a.a; p.b = a.b; p.M = a.M; p.N = a.N; p.K = a.K;
   p.bias = (const uint16_t*)a.bias; p.epilogue = a.epilogue;
   p.c = a.c; p.c_dtype = a.c_dtype; p.c_map = to_map(a.c_map); p.ldc = a.ldc;
   p.resid = a.resid; p.resid_dtype = a.resid_dtype; p.resid_map = to_map(a.resid_map);
   p.ld_resid = a.ld_resid; p.gate = a.gate; p.gate_stride = a.gate_stride;
   p.gate_sel = ModSel{0, 0, 0};
+  p.status = nullptr;
   return p;
 }
 
@@ -230,10 +231,13 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
   void* Kk = slot(XEMA_SLOT_K);
   void* VT = slot(XEMA_SLOT_VT);
   void* ln1 = slot(XEMA_SLOT_LN1);
-  void* qkv = slot(XEMA_SLOT_QKV);
-  void* wo16 = slot(XEMA_SLOT_WO16);
-  void* wup16 = slot(XEMA_SLOT_WUP16);
-  void* wdown16 = slot(XEMA_SLOT_WDOWN16);
+  void* qkv = slot(XEMA_SLOT_QKV);  // empty: the QKV GEMM writes the heads itself
+  // fp16 phase-B weights: the caller's (cfg.weights_f16) or this call's copies
+  const bool copy_w = c.weights_f16 == 0;
+  const void* wo16 = copy_w ? slot(XEMA_SLOT_WO16) : w.o_w;
+  const void* wup16 = copy_w ? slot(XEMA_SLOT_WUP16) : w.up_w;
+  const void* wdown16 = copy_w ? slot(XEMA_SLOT_WDOWN16) : w.down_w;
+  uint32_t* status = (uint32_t*)slot(XEMA_SLOT_STATUS);  // range flags, one word per kind
   void* attn = slot(XEMA_SLOT_ATTN);
   float* x1 = (float*)slot(XEMA_SLOT_X1);
   void* ln2 = slot(XEMA_SLOT_LN2);
@@ -250,9 +254,9 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
   const int64_t txt_delta = dual_stream(c) ? B * 6 * D : 0;
   auto sel_at = [&](int64_t t0) { return ModSel{t0, r.text_len, txt_delta}; };
 
-  // step 0
+  // step 0 (the first launch also clears the range flags)
   XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_w,
-                        (const uint16_t*)w.ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s));
+                        (const uint16_t*)w.ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s, status));
   if (dual_stream(c))
     XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_txt_w,
                           (const uint16_t*)w.ada_txt_b, (int)B, (int)Dc, (int)(6 * D),
@@ -261,12 +265,8 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
 
   // phase A: LN1 -> QKV -> QK-norm/RoPE scatter, per token chunk.  The QKV
   // GEMM's epilogue does the scatter itself (a head per wave at head dim 64,
-  // per two waves at 128), the qkv slot stays unused and the padding tokens
-  // are zeroed once.
-  const bool fused_heads = c.head_dim == 64 || c.head_dim == 128;
-  // the qkv slot is sized for the unfused path only (empty when fused)
-  if (!fused_heads && plan.slot_bytes[XEMA_SLOT_QKV] < 6 * B * std::min(ch, L) * D)
-    return XEMA_ERR_INVALID_ARG;
+  // per two waves at 128; the shape checks admit only these), so the qkv
+  // slot stays empty; the padding tokens are zeroed once.
   for (int64_t t0 = 0; t0 < L; t0 += ch) {
     const int64_t cc = std::min(ch, L - t0);
     const RowMap xmap{cc, L, t0};
@@ -275,21 +275,22 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     const QkRopeArgs qa = qk_args(c, r, qkv, (int)t0, (int)cc, w.q_gamma, w.k_gamma, rope, Q, Kk, VT);
     GemmParams g{};
     g.dtype = XEMA_BF16; g.a = ln1; g.b = w.qkv_w; g.M = B * cc; g.N = (int)(3 * D); g.K = (int)D;
-    g.bias = (const uint16_t*)w.qkv_b; g.epilogue =
-        !fused_heads ? XEMA_EPI_BIAS : c.head_dim == 64 ? EPI_QKV_HEADS : EPI_QKV_HEADS_128;
+    g.bias = (const uint16_t*)w.qkv_b;
+    g.epilogue = c.head_dim == 64 ? EPI_QKV_HEADS : EPI_QKV_HEADS_128;
     g.c = qkv; g.c_dtype = XEMA_F16; g.c_map = RowMap{cc, cc, 0}; g.ldc = 3 * D;
     g.qk = qa;
+    g.status = status + 0;
     XEMA_TRY(launch_gemm(g, s));
-    if (!fused_heads) XEMA_TRY(launch_qk_norm_rope(qa, c.head_dim, s));
   }
-  if (fused_heads)
-    XEMA_TRY(launch_qkv_pad(qk_args(c, r, qkv, 0, 0, w.q_gamma, w.k_gamma, rope, Q, Kk, VT),
-                            c.head_dim, (int)L, s));
+  XEMA_TRY(launch_qkv_pad(qk_args(c, r, qkv, 0, 0, w.q_gamma, w.k_gamma, rope, Q, Kk, VT),
+                          c.head_dim, (int)L, s));
 
-  // step 4: fp16 copies of the phase-B weights
-  XEMA_TRY(launch_convert_f16((const uint16_t*)w.o_w, (_Float16*)wo16, D * D, s));
-  XEMA_TRY(launch_convert_f16((const uint16_t*)w.up_w, (_Float16*)wup16, F * D, s));
-  XEMA_TRY(launch_convert_f16((const uint16_t*)w.down_w, (_Float16*)wdown16, D * F, s));
+  // step 4: fp16 copies of the phase-B weights, unless the caller passed them
+  if (copy_w) {
+    XEMA_TRY(launch_convert_f16((const uint16_t*)w.o_w, (_Float16*)wo16, D * D, s, status + 3));
+    XEMA_TRY(launch_convert_f16((const uint16_t*)w.up_w, (_Float16*)wup16, F * D, s, status + 3));
+    XEMA_TRY(launch_convert_f16((const uint16_t*)w.down_w, (_Float16*)wdown16, D * F, s, status + 3));
+  }
 
   // phase B: attention -> out-proj -> LN2 -> MLP, per query chunk
   auto attention_of = [&](int64_t t0, void* dst, hipStream_t q) {
@@ -314,13 +315,14 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
     if (used && hipEventRecord(used, s) != hipSuccess) return hipErrorLaunchFailure;
 
     hipError_t e = launch_ln_modulate(x1, XEMA_F32, ident, B * cc, (int)D, mod + 3 * D, mod + 4 * D,
-                                      6 * D, sel_at(t0), c.ln_eps, ln2, XEMA_F16, s);
+                                      6 * D, sel_at(t0), c.ln_eps, ln2, XEMA_F16, s, status + 1);
     if (e != hipSuccess) return e;
 
     GemmParams u{};
     u.dtype = XEMA_F16; u.a = ln2; u.b = wup16; u.M = B * cc; u.N = (int)F; u.K = (int)D;
     u.bias = (const uint16_t*)w.up_b; u.epilogue = XEMA_EPI_BIAS_GELU;
     u.c = hid; u.c_dtype = XEMA_F16; u.c_map = ident; u.ldc = F;
+    u.status = status + 2;
     if ((e = launch_gemm(u, s)) != hipSuccess) return e;
 
     GemmParams d{};
@@ -462,6 +464,25 @@ extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request*
                                   int64_t workspace_bytes, void* out, void* stream) {
   return block_fwd(cfg, req, tokens, w, cond, req ? req->batch : 1, chunk_tokens, workspace,
                    workspace_bytes, out, stream, nullptr);
+}
+
+extern "C" int xema_block_status(const xema_plan* plan, const void* workspace, void* stream,
+                                 uint32_t* flags) {
+  if (!plan || !workspace || !flags) return XEMA_ERR_INVALID_ARG;
+  if (plan->n_slots <= XEMA_SLOT_STATUS || plan->slot_bytes[XEMA_SLOT_STATUS] < 4 * XEMA_STATUS_WORDS ||
+      plan->slot_offset[XEMA_SLOT_STATUS] < 0)
+    return XEMA_ERR_INVALID_ARG;
+  uint32_t words[XEMA_STATUS_WORDS];
+  const hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(words, (const uint8_t*)workspace + plan->slot_offset[XEMA_SLOT_STATUS],
+                     sizeof(words), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return XEMA_ERR_HIP;
+  uint32_t f = 0;
+  for (int i = 0; i < XEMA_STATUS_WORDS; ++i)
+    if (words[i]) f |= 1u << i;
+  *flags = f;
+  return f ? XEMA_ERR_RANGE : XEMA_OK;
 }
 
 extern "C" int xema_dit_block_fwd_pipelined(const xema_block_cfg* cfg, const xema_request* req,

@@ -47,6 +47,16 @@ __device__ __forceinline__ float as_rounded_f32(float x) {
   return x;
 }
 
+// Whether v rounds to a finite fp16 value: |v| < 65520 (values from 65504
+// up round to 65504, from 65520 on to infinity); false for NaN.
+__device__ __forceinline__ bool fits_f16(float v) { return __builtin_fabsf(v) < 65520.0f; }
+
+// Range flag: the lanes that saw a value outside the fp16 range store 1 to
+// the flag word (a plain vector store; every writer stores the same value).
+__device__ __forceinline__ void raise_flag(uint32_t* flag, bool bad) {
+  if (flag != nullptr && bad) *(volatile uint32_t*)flag = 1u;
+}
+
 // Butterfly sum over the 64 lanes of a wave (fixed pairing order, so every
 // lane ends with the same, run-to-run reproducible value).
 __device__ __forceinline__ float wave_sum(float v) {

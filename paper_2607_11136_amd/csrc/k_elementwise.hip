@@ -20,9 +20,13 @@ __global__ __launch_bounds__(256) void k_adaln(const uint16_t* __restrict__ cond
                                                const uint16_t* __restrict__ w,
                                                const uint16_t* __restrict__ bias, int batch,
                                                int cond_dim, int out_dim,
-                                               float* __restrict__ mod) {
+                                               float* __restrict__ mod,
+                                               uint32_t* __restrict__ status_clear) {
   const int lane = threadIdx.x & 63;
   const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  // the block's range flags start clear (the first launch of every call)
+  if (status_clear != nullptr && blockIdx.x == 0 && threadIdx.x < XEMA_STATUS_WORDS)
+    status_clear[threadIdx.x] = 0u;
   if (n >= out_dim) return;
   const uint16_t* wrow = w + n * cond_dim;
   const float bn = bf16_bits_to_f32(bias[n]);
@@ -136,7 +140,8 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale,
                                                      int64_t mod_stride, ModSel sel, float eps,
-                                                     YT* __restrict__ y) {
+                                                     YT* __restrict__ y,
+                                                     uint32_t* __restrict__ status) {
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
@@ -169,6 +174,7 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
   const float* sh = shift + moff;
   const float* sc = scale + moff;
   YT* yr = y + r * dim;
+  bool bad = false;
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
     const int c = i * 64 * E + lane * E;
@@ -180,8 +186,13 @@ __global__ __launch_bounds__(256) void k_ln_modulate(const XT* __restrict__ x, R
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[4 * h + e] = fmaf(v[i][4 * h + e] * rstd, 1.0f + s4[e], h4[e]);
     }
+    if constexpr (__is_same(YT, f16)) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) bad |= !fits_f16(o[e]);
+    }
     store_e<YT, E>(yr + c, o);
   }
+  raise_flag(status, bad);
 }
 
 // ---------------------------------------------------------------------------
@@ -357,34 +368,39 @@ __global__ __launch_bounds__(256) void k_qk_norm_rope(QkRopeArgs a) {
 // Step 4: bf16 -> fp16 copy, 8 elements per thread per iteration.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_convert_f16(const uint16_t* __restrict__ src,
-                                                     f16* __restrict__ dst, int64_t n8) {
+                                                     f16* __restrict__ dst, int64_t n8,
+                                                     uint32_t* __restrict__ status) {
+  bool bad = false;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8;
        i += (int64_t)gridDim.x * 256) {
     const u32x4 u = reinterpret_cast<const u32x4*>(src)[i];
     f16x8 o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      o[2 * e] = (f16)__uint_as_float(u[e] << 16);
-      o[2 * e + 1] = (f16)__uint_as_float(u[e] & 0xffff0000u);
+      const float w0 = __uint_as_float(u[e] << 16), w1 = __uint_as_float(u[e] & 0xffff0000u);
+      bad |= !fits_f16(w0) || !fits_f16(w1);
+      o[2 * e] = (f16)w0;
+      o[2 * e + 1] = (f16)w1;
     }
     reinterpret_cast<f16x8*>(dst)[i] = o;
   }
+  raise_flag(status, bad);
 }
 
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_adaln(const uint16_t* cond, const uint16_t* w, const uint16_t* bias, int batch,
-                        int cond_dim, int out_dim, float* mod, hipStream_t s) {
+                        int cond_dim, int out_dim, float* mod, hipStream_t s, uint32_t* status_clear) {
   hipLaunchKernelGGL(k_adaln, dim3((out_dim + 3) / 4), dim3(256), 0, s, cond, w, bias, batch,
-                     cond_dim, out_dim, mod);
+                     cond_dim, out_dim, mod, status_clear);
   return hipGetLastError();
 }
 
 template <typename XT, typename YT>
 static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, const float* shift,
                               const float* scale, int64_t mod_stride, ModSel sel, float eps, YT* y,
-                              hipStream_t s) {
+                              hipStream_t s, uint32_t* status) {
   const dim3 grid((unsigned)((rows + 3) / 4));
   if constexpr (sizeof(XT) == 2) {
     if (dim % 512 == 0) {
@@ -392,7 +408,7 @@ static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, cons
 #define XEMA_LN_CASE(NS)                                                                        \
   case NS:                                                                                      \
     hipLaunchKernelGGL((k_ln_modulate<XT, YT, NS, 8>), grid, dim3(256), 0, s, x, m, rows, dim,   \
-                       shift, scale, mod_stride, sel, eps, y);                                  \
+                       shift, scale, mod_stride, sel, eps, y, status);                          \
     break;
         XEMA_LN_CASE(1) XEMA_LN_CASE(2) XEMA_LN_CASE(3) XEMA_LN_CASE(4) XEMA_LN_CASE(5)
         XEMA_LN_CASE(6) XEMA_LN_CASE(7) XEMA_LN_CASE(8) XEMA_LN_CASE(9) XEMA_LN_CASE(10)
@@ -409,7 +425,7 @@ static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, cons
 #define XEMA_LN_CASE(NS)                                                                      \
   case NS:                                                                                    \
     hipLaunchKernelGGL((k_ln_modulate<XT, YT, NS, 4>), grid, dim3(256), 0, s, x, m, rows, dim, \
-                       shift, scale, mod_stride, sel, eps, y);                                \
+                       shift, scale, mod_stride, sel, eps, y, status);                        \
     break;
     XEMA_LN_CASE(1) XEMA_LN_CASE(2) XEMA_LN_CASE(3) XEMA_LN_CASE(4) XEMA_LN_CASE(5)
     XEMA_LN_CASE(6) XEMA_LN_CASE(7) XEMA_LN_CASE(8) XEMA_LN_CASE(9) XEMA_LN_CASE(10)
@@ -427,15 +443,20 @@ static hipError_t launch_ln_t(const XT* x, RowMap m, int64_t rows, int dim, cons
 
 hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows, int dim,
                               const float* shift, const float* scale, int64_t mod_stride,
-                              ModSel sel, float eps, void* y, int y_dtype, hipStream_t s) {
+                              ModSel sel, float eps, void* y, int y_dtype, hipStream_t s,
+                              uint32_t* status) {
   if (x_dtype == XEMA_BF16 && y_dtype == XEMA_BF16)
-    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (bf16*)y, s);
+    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (bf16*)y, s,
+                       status);
   if (x_dtype == XEMA_BF16 && y_dtype == XEMA_F16)
-    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (f16*)y, s);
+    return launch_ln_t((const uint16_t*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (f16*)y, s,
+                       status);
   if (x_dtype == XEMA_F32 && y_dtype == XEMA_BF16)
-    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (bf16*)y, s);
+    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (bf16*)y, s,
+                       status);
   if (x_dtype == XEMA_F32 && y_dtype == XEMA_F16)
-    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (f16*)y, s);
+    return launch_ln_t((const float*)x, m, rows, dim, shift, scale, mod_stride, sel, eps, (f16*)y, s,
+                       status);
   return hipErrorInvalidValue;
 }
 
@@ -489,11 +510,11 @@ hipError_t launch_qk_norm_rope(const QkRopeArgs& a, int head_dim, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_convert_f16(const uint16_t* src, f16* dst, int64_t n, hipStream_t s) {
+hipError_t launch_convert_f16(const uint16_t* src, f16* dst, int64_t n, hipStream_t s, uint32_t* status) {
   const int64_t n8 = n / 8;
   const int64_t blocks = std::min<int64_t>((n8 + 255) / 256, 256 * 16);
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_convert_f16, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, n8);
+  hipLaunchKernelGGL(k_convert_f16, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, n8, status);
   return hipGetLastError();
 }
 

@@ -219,6 +219,7 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
 #pragma unroll
     for (int q = 0; q < 4; ++q) load4f<uint16_t>(bias + col0 + j * 32 + 8 * q, bv[j][q]);
 
+  bool bad = false;  // an fp16 result at or beyond the fp16 range
   if (sect < 2) {
     const uint16_t* gam = sect == 0 ? a.q_gamma : a.k_gamma;
     float g[NJ][4][4];
@@ -326,14 +327,18 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
             const float2 cs = make_float2(cc[2 * e2], cc[2 * e2 + 1]);
             const float u0 = v[j][q][2 * e2] * r * g[j][q][2 * e2];
             const float u1 = v[j][q][2 * e2 + 1] * r * g[j][q][2 * e2 + 1];
-            o[q][2 * e2] = (f16)as_rounded_f32(fmaf(u0, cs.x, -u1 * cs.y) * f);
-            o[q][2 * e2 + 1] = (f16)as_rounded_f32(fmaf(u0, cs.y, u1 * cs.x) * f);
+            const float y0 = as_rounded_f32(fmaf(u0, cs.x, -u1 * cs.y) * f);
+            const float y1 = as_rounded_f32(fmaf(u0, cs.y, u1 * cs.x) * f);
+            bad |= valid && (!fits_f16(y0) || !fits_f16(y1));
+            o[q][2 * e2] = (f16)y0;
+            o[q][2 * e2 + 1] = (f16)y1;
           }
         }
 #pragma unroll
         for (int q = 0; q < 4; q += 2) store_group_pair<f16>(row + j * 32 + 8 * q, o[q], o[q + 1], hi, valid);
       }
     }
+    raise_flag(p.status, bad);
     return;
   }
 
@@ -343,15 +348,20 @@ __device__ __forceinline__ void epilogue_qkv_heads(const GemmParams& p, const f3
   __syncthreads();
   f16* lds = reinterpret_cast<f16*>(smem) + wave * 64 * TPW;   // [64 dims][TPW tokens]
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int i = 0; i < MI; ++i) {
+    const bool valid = m0 + wm * (BM / 2) + i * 32 + r32 < m_end;
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          lds[(32 * j + 8 * q + 4 * hi + e) * TPW + i * 32 + r32] =
-              (f16)as_rounded_f32(acc[i][j][4 * q + e] + bv[j][q][e]);
+        for (int e = 0; e < 4; ++e) {
+          const float y = as_rounded_f32(acc[i][j][4 * q + e] + bv[j][q][e]);
+          bad |= valid && !fits_f16(y);
+          lds[(32 * j + 8 * q + 4 * hi + e) * TPW + i * 32 + r32] = (f16)y;
+        }
+  }
+  raise_flag(p.status, bad);
   __syncthreads();
   for (int it = lane; it < 64 * (TPW / 8); it += 64) {
     const int d = it / (TPW / 8), g8 = it % (TPW / 8);
@@ -568,6 +578,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
     for (int q = 0; q < 4; ++q)
       load4f<uint16_t>(bias + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, bv[j][q]);
   const int64_t rpb = p.c_map.rows_per_batch;
+  bool bad = false;  // an fp16 result at or beyond the fp16 range
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int64_t m = m0 + wm * (BM / 2) + i * 32 + r32;
@@ -622,8 +633,10 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
           c4 a, b;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            a[e] = from_f32<CT>(as_rounded_f32(v[j][q][e]));
-            b[e] = from_f32<CT>(as_rounded_f32(v[j][q + 1][e]));
+            const float y0 = as_rounded_f32(v[j][q][e]), y1 = as_rounded_f32(v[j][q + 1][e]);
+            if constexpr (__is_same(CT, f16)) bad |= !fits_f16(y0) || !fits_f16(y1);
+            a[e] = from_f32<CT>(y0);
+            b[e] = from_f32<CT>(y1);
           }
           store_group_pair<CT>(crow_ptr + n0 + wn * WN + j * 32 + 8 * q, a, b, hi, true);
         }
@@ -635,6 +648,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
           store4<CT>(crow_ptr + n0 + wn * WN + j * 32 + 8 * q + 4 * hi, v[j][q]);
     }
   }
+  raise_flag(p.status, bad);
 }
 
 // Rows [0, split) go in 256-row tiles, rows [split, M) in 128-row tiles.  The

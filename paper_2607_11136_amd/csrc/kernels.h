@@ -60,6 +60,7 @@ struct GemmParams {
   int64_t gate_stride;
   ModSel gate_sel;  // per-row choice of the gate vector (positions within c_map's rows)
   QkRopeArgs qk;    // EPI_QKV_HEADS: rows are tokens [qk.tok_begin, +c_map.rows_per_batch)
+  uint32_t* status; // range flag set when an fp16 output leaves the fp16 range (may be null)
 };
 
 // Internal epilogues of the QKV GEMM (steps a2 + a3 in one kernel): bias,
@@ -90,16 +91,22 @@ struct UpconvParams {
 hipError_t launch_upconv_prep(const uint16_t* w, int ci, int co, uint16_t* wp, hipStream_t s);
 hipError_t launch_upconv(const UpconvParams& p, hipStream_t s);
 
+// status_clear (may be null): XEMA_STATUS_WORDS range flags zeroed by the launch.
 hipError_t launch_adaln(const uint16_t* cond, const uint16_t* w, const uint16_t* bias, int batch,
-                        int cond_dim, int out_dim, float* mod, hipStream_t s);
+                        int cond_dim, int out_dim, float* mod, hipStream_t s,
+                        uint32_t* status_clear = nullptr);
+// status (may be null): set when an fp16 output leaves the fp16 range.
 hipError_t launch_ln_modulate(const void* x, int x_dtype, RowMap m, int64_t rows, int dim,
                               const float* shift, const float* scale, int64_t mod_stride,
-                              ModSel sel, float eps, void* y, int y_dtype, hipStream_t s);
+                              ModSel sel, float eps, void* y, int y_dtype, hipStream_t s,
+                              uint32_t* status = nullptr);
 hipError_t launch_rope_table(RopeGeom g, float theta, float* table, hipStream_t s);
 hipError_t launch_qk_norm_rope(const QkRopeArgs& a, int head_dim, hipStream_t s);
 // Zeros for the padding tokens [L, Lp) of Q, K and V^T (all batch rows, heads).
 hipError_t launch_qkv_pad(const QkRopeArgs& a, int head_dim, int seq_len, hipStream_t s);
-hipError_t launch_convert_f16(const uint16_t* src, _Float16* dst, int64_t n, hipStream_t s);
+// status (may be null): set when a converted value leaves the fp16 range.
+hipError_t launch_convert_f16(const uint16_t* src, _Float16* dst, int64_t n, hipStream_t s,
+                              uint32_t* status = nullptr);
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, int head_dim, hipStream_t s);
 

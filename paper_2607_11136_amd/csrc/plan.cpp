@@ -90,6 +90,7 @@ int validate_shapes(const xema_block_cfg* cfg, const xema_request* req) {
   if (rope_sum > c.head_dim) return XEMA_ERR_INVALID_ARG;
   if (!(c.rope_theta > 0.f) || !(c.ln_eps > 0.f) || !(c.qk_eps > 0.f)) return XEMA_ERR_INVALID_ARG;
   if (c.modulation_streams < 0 || c.modulation_streams > 2) return XEMA_ERR_INVALID_ARG;
+  if (c.weights_f16 != 0 && c.weights_f16 != 1) return XEMA_ERR_INVALID_ARG;
   const int64_t L = seq_len(r);
   if (L <= 0) return XEMA_ERR_INVALID_ARG;
   // what the kernels handle
@@ -117,6 +118,7 @@ int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t
   const int64_t L = seq_len(req);
   const int64_t lp = padded_len(L);
   const bool chunked = c < L;
+  const int64_t copies = cfg.weights_f16 ? 0 : 1;  // fp16 weight copies made by the call
   struct Spec { int64_t bytes; int begin, end; };
   const Spec spec[XEMA_NUM_SLOTS] = {
       {24 * B * D * (dual_stream(cfg) ? 2 : 1), 0, 10},  // XEMA_SLOT_MOD
@@ -125,14 +127,15 @@ int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t
       {2 * B * D * lp, 1, 10},                     // XEMA_SLOT_K
       {2 * B * D * lp, 1, 10},                     // XEMA_SLOT_VT
       {2 * B * c * D, 1, 3},                       // XEMA_SLOT_LN1
-      {cfg.head_dim == 64 || cfg.head_dim == 128 ? 0 : 6 * B * c * D, 2, 4},  // XEMA_SLOT_QKV (unused when fused)
-      {2 * D * D, 4, 10},                          // XEMA_SLOT_WO16
-      {2 * F * D, 4, 10},                          // XEMA_SLOT_WUP16
-      {2 * D * F, 4, 10},                          // XEMA_SLOT_WDOWN16
+      {0, 2, 4},                                   // XEMA_SLOT_QKV: the QKV GEMM writes the heads itself
+      {copies * 2 * D * D, 4, 10},                 // XEMA_SLOT_WO16
+      {copies * 2 * F * D, 4, 10},                 // XEMA_SLOT_WUP16
+      {copies * 2 * D * F, 4, 10},                 // XEMA_SLOT_WDOWN16
       {2 * B * c * D, 5, chunked ? 10 : 7},        // XEMA_SLOT_ATTN
       {4 * B * c * D, 6, 10},                      // XEMA_SLOT_X1
       {2 * B * c * D, 7, 9},                       // XEMA_SLOT_LN2
       {2 * B * c * F, 8, 10},                      // XEMA_SLOT_HID
+      {4 * XEMA_STATUS_WORDS, 0, 10},              // XEMA_SLOT_STATUS
   };
   std::vector<Rect> rects;
   for (int i = 0; i < XEMA_NUM_SLOTS; ++i)
@@ -286,6 +289,7 @@ extern "C" const char* xema_status_str(int status) {
     case XEMA_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
     case XEMA_ERR_MISALIGNED: return "misaligned pointer";
     case XEMA_ERR_HIP: return "HIP error";
+    case XEMA_ERR_RANGE: return "an fp16 intermediate left its range";
     default: return "unknown status";
   }
 }

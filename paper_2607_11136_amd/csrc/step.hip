@@ -181,7 +181,7 @@ extern "C" int xema_dit_step_fwd(const xema_block_cfg* cfg, const xema_request* 
     if (plan->offloaded[i]) continue;  // host memory cannot alias device buffers
     for (int t = 0; t < kWeightTensors; ++t) {
       const void* p = tensor(weights[i], t);
-      if (wb[t] && overlaps(out, out_bytes, p, wb[t]) || overlaps(workspace, workspace_bytes, p, wb[t]))
+      if (wb[t] && (overlaps(out, out_bytes, p, wb[t]) || overlaps(workspace, workspace_bytes, p, wb[t])))
         return XEMA_ERR_INVALID_ARG;
     }
   }

@@ -35,7 +35,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = X.lib()
     declared = _declared_symbols()
-    assert len(declared) == 23, declared
+    assert len(declared) == 24, declared
     for name in declared:
         assert hasattr(lib, name), name
     assert declared == set(X.EXPORTED)
@@ -52,7 +52,7 @@ def test_layout_matches_oracle(name):
     for chunk in sorted({0, 1, 64, 100, 256, 2048, 8192} | set(s.chunks)):
         p = X.xema_workspace_layout(_cfg(s), _req(s), chunk)
         ts = OL.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, chunk,
-                              s.modulation_streams, s.head_dim)
+                              s.modulation_streams)
         offs, peak = OL.static_layout(ts)
         assert p.n_slots == len(ts) == len(X.SLOT_NAMES)
         assert p.workspace_bytes == peak
@@ -274,9 +274,11 @@ def test_op_validation():
     g = X.gemm_args(X.XEMA_F16, f, 100, 256, f, 256, f, X.XEMA_EPI_GATED_RESIDUAL, f + (1 << 30),
                     X.XEMA_F16, 256, resid=f, ld_resid=256, gate=f)
     assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_UNSUPPORTED
-    # the fused QKV-heads epilogue (code 3) is internal to the block forward
-    g = X.gemm_args(X.XEMA_BF16, f, 100, 256, f, 256, f, 3, f + (1 << 30), X.XEMA_F16, 256)
-    assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_INVALID_ARG
+    # the fused QKV-heads epilogues (codes 3 and 4, head dims 64 and 128) are
+    # internal to the block forward
+    for code in (3, 4):
+        g = X.gemm_args(X.XEMA_BF16, f, 100, 256, f, 256, f, code, f + (1 << 30), X.XEMA_F16, 256)
+        assert L.xema_op_gemm(ctypes.byref(g), None) == X.XEMA_ERR_INVALID_ARG, code
     # LN: dim not a multiple of 256
     assert L.xema_op_ln_modulate(f, X.XEMA_BF16, X.rowmap(4, 4, 0), 4, 300, f, f, 1800, 1e-6, f,
                                  X.XEMA_BF16, None) == X.XEMA_ERR_UNSUPPORTED

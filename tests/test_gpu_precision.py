@@ -1,0 +1,124 @@
+"""The block's precision contract on the GPU (xema.h, "Precision contract"):
+
+* phase-B weights handed over in fp16 (cfg.weights_f16) give the bytes of
+  the per-call conversion;
+* inputs at realistic large magnitudes (tokens x100, AdaLN scales up to
+  about +-50, every weight matrix x8) stay inside the fp16 range of the
+  intermediates and within the parity bar, scaled to the output's size;
+* an fp16 intermediate pushed out of its range raises the matching flag of
+  xema_block_status instead of passing silently.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_11136_amd as X
+import workloads as W
+from oracle import block as O
+
+from gpu_util import MAE, MAX_REL, Device, errors, slot_view
+
+pytestmark = pytest.mark.gpu
+
+D64 = W.tiny_shape(name="prec_d64", cfg_id=70, batch=2, text_len=45, grid=(3, 9, 23), hidden=512, heads=8,
+                   head_dim=64, mlp_hidden=2048, cond_dim=512, rope_dims=(16, 24, 24))
+D128 = W.tiny_shape(name="prec_d128", cfg_id=71, batch=1, text_len=64, grid=(1, 20, 31), hidden=512, heads=4,
+                    head_dim=128, mlp_hidden=1536, cond_dim=256, rope_dims=(0, 64, 64))
+MATRICES = ("qkv_w", "o_w", "up_w", "down_w")
+
+
+def _f32(bits):
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def _scaled(bits, factor):
+    """bf16 bit patterns of bf16(value * factor)."""
+    return W.to_bf16_bits(_f32(bits) * np.float32(factor))
+
+
+@pytest.mark.parametrize("shape", [D64, D128], ids=lambda s: s.name)
+def test_fp16_weights_give_the_same_bytes(shape):
+    inp = W.make_inputs(shape)
+    base = Device(inp)
+    want, _, plan_bf16 = base.run(0)
+    pre = Device(W.Inputs(shape.with_(weights_f16=1), inp.x, inp.cond, inp.weights))
+    for chunk in (0, 100):
+        got, _, plan = pre.run(chunk)
+        assert torch.equal(got, want), chunk
+        for n in ("wo16", "wup16", "wdown16"):
+            assert plan.slots()[n][1] == 0
+    assert plan_bf16.workspace_bytes > X.xema_workspace_layout(pre.cfg, pre.req, 0).workspace_bytes
+
+
+def _large(shape):
+    """Tokens x100, the AdaLN rows of scale1 and scale2 x12.5 (the scales
+    then reach about +-45), and every weight matrix x8."""
+    inp = W.make_inputs(shape)
+    D = shape.hidden
+    w = dict(inp.weights)
+    for n in MATRICES:
+        w[n] = _scaled(w[n], 8.0)
+    for part in (1, 4):   # scale1, scale2
+        rows = slice(part * D, (part + 1) * D)
+        aw, ab = w["ada_w"].copy(), w["ada_b"].copy()
+        aw[rows] = _scaled(aw[rows], 12.5)
+        ab[rows] = _scaled(ab[rows], 12.5)
+        w["ada_w"], w["ada_b"] = aw, ab
+    return W.Inputs(shape, _scaled(inp.x, 100.0), inp.cond, w)
+
+
+@pytest.mark.parametrize("shape", [D64, D128], ids=lambda s: s.name)
+def test_large_magnitudes_stay_in_range_and_tolerance(shape):
+    """The bar in the form that does not depend on the output's scale: max
+    rel is unchanged (|g - o| / max(|o|, 1)) and the mean absolute error is
+    held to 2e-3 times the mean |o| (the unit-scale bar, 2e-3, is about
+    1.4e-3 of the mean |o| of 1.4 there)."""
+    inp = _large(shape)
+    dev = Device(inp)
+    out, ws, plan = dev.run(0)
+    B, L, H, d = shape.batch, shape.seq_len, shape.heads, shape.head_dim
+    vt = slot_view(ws, plan, "vt", torch.float16, (B, H, d, X.padded_len(L))).float()
+    m = O.adaln_modulation(inp.f64("cond"), inp.weights_f64()["ada_w"], inp.weights_f64()["ada_b"])
+    ref = O.block_forward_shape(inp)
+    e = errors(out.cpu().numpy(), ref)
+    mean_o = float(np.abs(ref).mean())
+    print(f"{shape.name} large: max|scale| {np.abs(m[:, shape.hidden:2 * shape.hidden]).max():.1f}, "
+          f"max|V| {vt.abs().max().item():.1f}, mean|o| {mean_o:.1f}, {e}", flush=True)
+    assert np.abs(m[:, shape.hidden:2 * shape.hidden]).max() > 30
+    assert np.all(np.isfinite(out.cpu().numpy()))
+    assert e["max_rel"] <= MAX_REL and e["mae"] <= MAE * max(1.0, mean_o), e
+
+
+def _overflow_case(kind):
+    inp = W.make_inputs(D64)
+    D, w = D64.hidden, dict(inp.weights)
+    if kind == "qkv":      # V rows of W_qkv x1e5: V far beyond 65504
+        wq = w["qkv_w"].copy()
+        wq[2 * D:] = _scaled(wq[2 * D:], 1e5)
+        w["qkv_w"] = wq
+    elif kind == "ln2":    # scale2 about 1e6: h2 beyond the fp16 range
+        aw = w["ada_w"].copy()
+        aw[4 * D:5 * D] = _scaled(aw[4 * D:5 * D], 1e6)
+        w["ada_w"] = aw
+    elif kind == "mlp":    # W_up x1e5: the GELU outputs overflow
+        w["up_w"] = _scaled(w["up_w"], 1e5)
+    elif kind == "weights":  # one W_o entry of 1e5 cannot be converted to fp16
+        wo = w["o_w"].copy()
+        wo[3, 5] = W.to_bf16_bits(np.float32([1e5]))[0]
+        w["o_w"] = wo
+    return W.Inputs(D64, inp.x, inp.cond, w)
+
+
+@pytest.mark.parametrize("kind,bit", [("qkv", X.XEMA_RANGE_QKV), ("ln2", X.XEMA_RANGE_LN2),
+                                      ("mlp", X.XEMA_RANGE_MLP), ("weights", X.XEMA_RANGE_WEIGHTS)])
+def test_out_of_range_intermediate_raises_its_flag(kind, bit):
+    dev = Device(_overflow_case(kind))
+    for chunk in (0, 64):
+        out, ws, plan = dev.run(chunk, check_status=False)
+        flags = X.xema_block_status(plan, ws)
+        print(f"overflow {kind} chunk={chunk}: flags {flags:#x}", flush=True)
+        assert flags & bit, (kind, flags)
+    # the next clean call on the same workspace clears the flags
+    clean = Device(W.make_inputs(D64))
+    out, ws2, plan = clean.run(0, ws=ws)
+    assert X.xema_block_status(plan, ws2) == 0

@@ -110,11 +110,12 @@ def test_against_brute_force_optimum():
 def test_block_slot_table_reaches_max_live_bound(name):
     s = W.CONFIGS[name]
     for c in {0, 64, 256, 2048, 8192} | set(s.chunks):
-        ts = L.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, c,
-                             s.modulation_streams, s.head_dim)
-        offs, peak = L.static_layout(ts)
-        _check_valid(ts, offs, peak)
-        assert peak == L.max_live_bytes(ts), (name, c)
+        for wf16 in (0, 1):
+            ts = L.block_tensors(s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.grid, s.rope_dims, c,
+                                 s.modulation_streams, wf16)
+            offs, peak = L.static_layout(ts)
+            _check_valid(ts, offs, peak)
+            assert peak == L.max_live_bytes(ts), (name, c, wf16)
 
 
 def test_plan_is_largest_fitting_chunk_and_monotone():

@@ -433,25 +433,31 @@ def test_p13_zero_gates_of_one_stream_pass_its_tokens_through(stream):
     assert np.min(np.max(np.abs(out[:, moved] - x[:, moved]), axis=-1)) > 1e-3
 
 
-def _mut_rows_swapped(cond, w, text_len, L):
+def _sel(L, rows):
+    return np.arange(L) if rows is None else np.asarray(rows)
+
+
+def _mut_rows_swapped(cond, w, text_len, L, rows=None):
     m = O.adaln_modulation(cond, w["ada_w"], w["ada_b"])
     t = O.adaln_modulation(cond, w["ada_txt_w"], w["ada_txt_b"])
-    rows = np.repeat(t[:, None, :], L, axis=1)
-    rows[:, :text_len, :] = m[:, None, :]
-    return rows
+    sel = _sel(L, rows)
+    out = np.repeat(t[:, None, :], sel.size, axis=1)
+    out[:, sel < text_len, :] = m[:, None, :]
+    return out
 
 
-def _mut_rows_boundary(cond, w, text_len, L):
+def _mut_rows_boundary(cond, w, text_len, L, rows=None):
     m = O.adaln_modulation(cond, w["ada_w"], w["ada_b"])
     t = O.adaln_modulation(cond, w["ada_txt_w"], w["ada_txt_b"])
-    rows = np.repeat(m[:, None, :], L, axis=1)
-    rows[:, :text_len + 1, :] = t[:, None, :]
-    return rows
+    sel = _sel(L, rows)
+    out = np.repeat(m[:, None, :], sel.size, axis=1)
+    out[:, sel < text_len + 1, :] = t[:, None, :]
+    return out
 
 
-def _mut_rows_text_ignored(cond, w, text_len, L):
+def _mut_rows_text_ignored(cond, w, text_len, L, rows=None):
     m = O.adaln_modulation(cond, w["ada_w"], w["ada_b"])
-    return np.repeat(m[:, None, :], L, axis=1)
+    return np.repeat(m[:, None, :], _sel(L, rows).size, axis=1)
 
 
 @pytest.mark.parametrize("fn", [_mut_rows_swapped, _mut_rows_boundary, _mut_rows_text_ignored])

@@ -55,6 +55,7 @@ class BlockShape:
     qk_eps: float = 1e-6
     chunks: Tuple[int, ...] = (0,)      # chunk_tokens values exercised; 0 = all
     modulation_streams: int = 1         # 2: text tokens have their own AdaLN map
+    weights_f16: int = 0                # 1: W_o, W_up, W_down handed over in fp16
 
     @property
     def n_visual(self) -> int:
