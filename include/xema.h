@@ -302,12 +302,13 @@ XEMA_API int xema_dit_block_fwd_pipelined(const xema_block_cfg* cfg, const xema_
                                  void* out, void* stream, void* aux_stream);
 
 /* Range status of the last block call that used this workspace with this
- * layout (any xema_dit_block_fwd* entry point): waits for `stream`, copies
- * the status slot to the host and sets *flags to the XEMA_RANGE_* bits of
- * the fp16 intermediates that left their range (0: none).  Returns XEMA_OK
- * when *flags is 0 and XEMA_ERR_RANGE otherwise; XEMA_ERR_INVALID_ARG for
- * NULL pointers or a layout without a status slot; XEMA_ERR_HIP if the copy
- * fails.  Synchronous; allocates nothing.                                 */
+ * layout (any xema_dit_block_fwd* entry point; workspace NULL: the static
+ * arena of xema_dit_block_fwd_static on the current device): waits for
+ * `stream`, copies the status slot to the host and sets *flags to the
+ * XEMA_RANGE_* bits of the fp16 intermediates that left their range (0:
+ * none).  Returns XEMA_OK when *flags is 0 and XEMA_ERR_RANGE otherwise;
+ * XEMA_ERR_INVALID_ARG for NULL plan or flags or a layout without a status
+ * slot; XEMA_ERR_HIP if the copy fails.  Synchronous; allocates nothing.  */
 XEMA_API int xema_block_status(const xema_plan* plan, const void* workspace, void* stream,
                                uint32_t* flags);
 

@@ -157,6 +157,8 @@ _SIGNATURES = {
                                                     ctypes.POINTER(BlockWeights), _P, _I32, _I32, _P, _I64, _P,
                                                     _P, _P]),
     "xema_block_status": (ctypes.c_int, [ctypes.POINTER(Plan), _P, _P, ctypes.POINTER(ctypes.c_uint32)]),
+    "xema_dit_block_fwd_static": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
+                                                 ctypes.POINTER(BlockWeights), _P, _I32, _P, _P]),
     "xema_vae_upconv_weight_bytes": (ctypes.c_int, [_I32, _I32, ctypes.POINTER(_I64)]),
     "xema_vae_upconv_prepare": (ctypes.c_int, [_P, _I32, _I32, _P, _P]),
     "xema_vae_upconv": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _I32, _I32, _I32, _P, _P]),
@@ -305,6 +307,18 @@ def xema_block_status(plan: Plan, workspace, stream=None) -> int:
     if st not in (XEMA_OK, XEMA_ERR_RANGE):
         raise XemaError(st, "xema_block_status")
     return flags.value
+
+
+XEMA_STATIC_ARENA_BYTES = 64 << 20
+
+
+def xema_dit_block_fwd_static(cfg: BlockCfg, req: Request, tokens, weights: BlockWeights, cond,
+                              chunk_tokens: int, out, stream=None) -> None:
+    """The block forward with its arena in the library's static device array
+    (no workspace, no allocation; xema_static.h)."""
+    _check(lib().xema_dit_block_fwd_static(ctypes.byref(cfg), ctypes.byref(req), _ptr(tokens),
+                                           ctypes.byref(weights), _ptr(cond), chunk_tokens, _ptr(out),
+                                           _stream(stream)), "xema_dit_block_fwd_static")
 
 
 def xema_workspace_plan_serial(cfg: BlockCfg, req: Request, budget_bytes: int):

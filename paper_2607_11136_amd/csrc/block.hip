@@ -416,10 +416,10 @@ static int check_block_call(const xema_block_cfg* cfg, const xema_request* req, 
   return XEMA_OK;
 }
 
-static int block_fwd(const xema_block_cfg* cfg, const xema_request* req, const void* tokens,
-                     const xema_block_weights* w, const void* cond, int32_t batch_group,
-                     int32_t chunk_tokens, void* workspace, int64_t workspace_bytes, void* out,
-                     void* stream, void* aux_stream) {
+int xema::block_fwd(const xema_block_cfg* cfg, const xema_request* req, const void* tokens,
+                    const xema_block_weights* w, const void* cond, int32_t batch_group,
+                    int32_t chunk_tokens, void* workspace, int64_t workspace_bytes, void* out,
+                    void* stream, void* aux_stream) {
   int st = check_block_call(cfg, req, tokens, w, cond, workspace, workspace_bytes, out);
   if (st != XEMA_OK) return st;
   if (batch_group < 1) return XEMA_ERR_INVALID_ARG;
@@ -468,7 +468,13 @@ extern "C" int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request*
 
 extern "C" int xema_block_status(const xema_plan* plan, const void* workspace, void* stream,
                                  uint32_t* flags) {
-  if (!plan || !workspace || !flags) return XEMA_ERR_INVALID_ARG;
+  if (!plan || !flags) return XEMA_ERR_INVALID_ARG;
+  if (!workspace) {  // the static arena of xema_dit_block_fwd_static on this device
+    void* a = nullptr;
+    const int st = static_arena(&a);
+    if (st != XEMA_OK) return st;
+    workspace = a;
+  }
   if (plan->n_slots <= XEMA_SLOT_STATUS || plan->slot_bytes[XEMA_SLOT_STATUS] < 4 * XEMA_STATUS_WORDS ||
       plan->slot_offset[XEMA_SLOT_STATUS] < 0)
     return XEMA_ERR_INVALID_ARG;

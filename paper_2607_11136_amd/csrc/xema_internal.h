@@ -40,6 +40,18 @@ inline const void* const* weight_ptrs(const xema_block_weights& w) { return &w.a
 inline const void** weight_ptrs(xema_block_weights& w) { return &w.ada_w; }
 static_assert(sizeof(xema_block_weights) == kWeightTensors * sizeof(void*), "weight struct layout");
 
+// The block forward behind every xema_dit_block_fwd* entry point: validates
+// the call (the workspace must hold the layout of a batch_group-sequence
+// request at chunk_tokens), then runs the groups; aux_stream as in
+// xema_dit_block_fwd_pipelined.
+int block_fwd(const xema_block_cfg* cfg, const xema_request* req, const void* tokens,
+              const xema_block_weights* w, const void* cond, int32_t batch_group, int32_t chunk_tokens,
+              void* workspace, int64_t workspace_bytes, void* out, void* stream, void* aux_stream);
+
+// Address of the current device's static arena (xema_static.h), looked up
+// once per device.  XEMA_ERR_HIP if it cannot be obtained.
+int static_arena(void** ptr);
+
 }  // namespace xema
 
 #ifdef __HIPCC__

@@ -26,7 +26,7 @@ def _req(s: W.BlockShape):
 
 def _declared_symbols():
     names = set()
-    for h in ("xema.h", "xema_ops.h", "xema_step.h", "xema_vae.h"):
+    for h in ("xema.h", "xema_ops.h", "xema_step.h", "xema_vae.h", "xema_static.h"):
         src = open(os.path.join(ROOT, "include", h)).read()
         names.update(re.findall(r"XEMA_API\s+[\w\s\*]+?\b(xema_\w+)\s*\(", src))
     return names
@@ -35,7 +35,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = X.lib()
     declared = _declared_symbols()
-    assert len(declared) == 24, declared
+    assert len(declared) == 25, declared
     for name in declared:
         assert hasattr(lib, name), name
     assert declared == set(X.EXPORTED)
