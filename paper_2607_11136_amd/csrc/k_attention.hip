@@ -19,7 +19,7 @@
 // kernels differ in how they detect that and in their schedule:
 //   k_attention (used at d = 128): the reference max enters as the
 //     accumulator input of the score MFMA, the trigger is the sum of a tile's
-//     P exceeding PMAX = 2^12 (a v_dot2 over the packed fp16 P, which is also
+//     P exceeding PMAX = 2^12 (the sum of the packed fp16 P, which is also
 //     the row sum), two wave groups run offset by a phase over a 3-stage LDS
 //     ring so one group's softmax overlaps the other's MFMAs;
 //   k_attention_lazy (used at d = 64): two column blocks per wave (half the
@@ -100,14 +100,19 @@ __device__ __forceinline__ int swz_v(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // P = 2^(s - shift) for the 32 scores a lane holds for one query column,
-// packed to fp16 as the B operand of the P V^T product; returns the sum of the
-// packed fp16 values (v_dot2 with (1, 1), fp32 accumulation), so the row sum
-// is taken over exactly the P that multiplies V.
+// packed to fp16 as the B operand of the P V^T product; returns the sum of
+// the packed fp16 values.  The pairs are added as packed fp16 into two
+// partial sums of eight pairs each, which two v_dot2 with (1, 1) add in fp32:
+// a chain of sixteen v_dot2 per column, one per pair, cost about 5% of the
+// kernel on the video workload and overlapped nothing.  The fp16 additions
+// round with relative error 2^-11 each (the tile's sum enters the row sum and
+// the rescale trigger; a P that overflows fp16 still makes the sum
+// infinite).
 template <bool SHIFT>
 __device__ __forceinline__ float exp_pack(const f32x16& s0, const f32x16& s1, float shift,
                                           f16x8 (&pf)[2][2]) {
   const f16x2 one = {(f16)1.f, (f16)1.f};
-  float acc = 0.f;
+  f16x2 part[2] = {{(f16)0.f, (f16)0.f}, {(f16)0.f, (f16)0.f}};
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -118,11 +123,11 @@ __device__ __forceinline__ float exp_pack(const f32x16& s0, const f32x16& s1, fl
         const float x0 = SHIFT ? sv[8 * u + e] - shift : sv[8 * u + e];
         const float x1 = SHIFT ? sv[8 * u + e + 1] - shift : sv[8 * u + e + 1];
         const f16x2 h = {(f16)fast_exp2(x0), (f16)fast_exp2(x1)};
-        acc = __builtin_amdgcn_fdot2(h, one, acc, false);
+        part[(e >> 1) & 1] += h;
         pf[kb][u][e] = h[0];
         pf[kb][u][e + 1] = h[1];
       }
-  return acc;
+  return __builtin_amdgcn_fdot2(part[1], one, __builtin_amdgcn_fdot2(part[0], one, 0.f, false), false);
 }
 
 // Queue the K and V^T tiles of one key tile into one LDS stage (this wave's
@@ -267,7 +272,7 @@ __device__ __forceinline__ void tile_softmax(const f32x16 (&s)[2][QB], bool firs
 
 // Online softmax for k_attention_lazy.  The scores arrive as s - mrow (the
 // extra k-step of scores_col), so the common path packs P = 2^s straight
-// from the MFMA output; its v_dot2 sum is the row sum.  A column grows when
+// from the MFMA output; its sum (exp_pack) is the row sum.  A column grows when
 // the larger of its two lanes' sums exceeds PMAX (a P that overflows fp16
 // makes its sum infinite, so it always grows) and on the first tile; then
 // rescale_col moves mrow to the tile max, rounded to fp16 because it feeds
