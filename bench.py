@@ -53,10 +53,16 @@ def bench_gpu(args, shape):
 
     x, cond = up(inp.x), up(inp.cond)
     w = {k: up(v) for k, v in inp.weights.items()}
+    weights_f16 = 0 if args.bf16_weights else 1
+    if weights_f16:
+        # W_o, W_up, W_down in fp16, converted once per model as a serving
+        # process would at load (the block then reads them directly)
+        for k in ("o_w", "up_w", "down_w"):
+            w[k] = w[k].to(torch.float16)
     weights = X.block_weights(w)
     cfg = X.block_cfg(shape.hidden, shape.heads, shape.head_dim, shape.mlp_hidden, shape.cond_dim,
                       shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps,
-                      shape.modulation_streams)
+                      shape.modulation_streams, weights_f16)
     req = X.request(shape.batch, shape.text_len, *shape.grid)
     if args.chunk is not None:
         group = args.batch_group or shape.batch
@@ -132,6 +138,7 @@ def bench_gpu(args, shape):
         "plan": plan,
         "batch_group": group,
         "device_peak_bytes": int(torch.cuda.max_memory_allocated()),
+        "weights_f16": weights_f16,
     }
 
 
@@ -335,8 +342,9 @@ def bench_vae(args):
 
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attention_video_hbm_traffic.md")
+# the files the attention kernel is built from
 TRAFFIC_SOURCES = ("paper_2607_11136_amd/csrc/k_attention.hip", "paper_2607_11136_amd/csrc/device_common.h",
-                   "paper_2607_11136_amd/csrc/kernels.h")
+                   "paper_2607_11136_amd/csrc/attention.h")
 
 
 def attention_source_digest():
@@ -433,6 +441,9 @@ def main():
                     help="device weight budget in bytes; the plan picks the smallest K (step mode)")
     ap.add_argument("--staging", type=int, default=2, help="device staging slots (step mode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--bf16-weights", action="store_true",
+                    help="hand W_o, W_up, W_down over in bf16 (converted into the arena on every call) "
+                         "instead of fp16 converted once")
     ap.add_argument("--one-stream", action="store_true",
                     help="run chunked phase B on one stream (no attention/projection overlap)")
     ap.add_argument("--vae", default=None, help="time the VAE upsampling stage vae_video or vae_1080p instead")
@@ -489,6 +500,8 @@ def main():
             "budget_bytes": args.budget, "chunk_tokens": plan.chunk_tokens, "batch_group": g["batch_group"],
             "phase_b_streams": 1 if args.one_stream or plan.chunk_tokens >= shape.seq_len else 2,
             "arena_bytes": plan.workspace_bytes, "device_peak_bytes": g["device_peak_bytes"],
+            "phase_b_weights": ("fp16, converted once per model" if g["weights_f16"]
+                                else "bf16, converted to fp16 in every call"),
         },
         "roofline": {
             "kernel": (f"{'k_attention_lazy<64>' if d == 64 else 'k_attention<128>'} (joint attention, "

@@ -49,8 +49,8 @@
 // Workgroups: NW = 8 waves = 8 * QB * 32 queries of one (batch, head).  The
 // grid is 1-D and remapped so that all query blocks of a head run on one XCD
 // and share its L2 copy of K and V.
+#include "attention.h"
 #include "device_common.h"
-#include "kernels.h"
 
 namespace xema {
 

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "attention.h"
 #include "xema_ops.h"
 
 namespace xema {
@@ -70,14 +71,6 @@ struct GemmParams {
 constexpr int EPI_QKV_HEADS = 3;
 constexpr int EPI_QKV_HEADS_128 = 4;
 
-struct AttnParams {
-  const _Float16* q;
-  const _Float16* k;
-  const _Float16* vt;
-  _Float16* o;
-  int batch, heads, seq_len, padded_len, q_begin, q_count;
-};
-
 // The VAE decoder's fused upsampling stage (k_upconv.hip).
 struct UpconvParams {
   const uint16_t* x;     // bf16 [n, h, w, ci]
@@ -108,6 +101,5 @@ hipError_t launch_qkv_pad(const QkRopeArgs& a, int head_dim, int seq_len, hipStr
 hipError_t launch_convert_f16(const uint16_t* src, _Float16* dst, int64_t n, hipStream_t s,
                               uint32_t* status = nullptr);
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
-hipError_t launch_attention(const AttnParams& p, int head_dim, hipStream_t s);
 
 }  // namespace xema
