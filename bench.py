@@ -315,7 +315,7 @@ def bench_vae(args):
         context = {"torch_unfused_ms": round(c0.elapsed_time(c1) / 3, 3),
                    "torch_unfused_extra_peak_bytes": int(torch.cuda.max_memory_allocated() - base)}
     flops = s.flops()                      # the definition: 3x3 over the upsampled image
-    mfma_flops = flops * 16 // 36          # what the phase form executes
+    mfma_flops = flops * 32 // 36          # what the phase form executes (hi and lo weights)
     up_bytes = s.n * 4 * s.h * s.w * s.ci * 2
     result = {
         "metric": "VAE upsampling stage ms (nearest 2x + 3x3 conv, fused)",

@@ -16,15 +16,18 @@
  * with U zero outside the 2H x 2W image.  The fused kernel computes y from x
  * directly: the upsampled image U (as large as y) is never stored, and each
  * output phase (parity of u and v) is a 2x2 convolution of x with weights
- * summed over the 3x3 taps that land on the same source pixel, 16/36 of the
+ * summed over the 3x3 taps that land on the same source pixel.  Each summed
+ * weight is kept as two bf16 values, hi + lo, both applied: 32/36 of the
  * convolution's multiply-adds.  A call may cover a band of source rows, so a
  * caller can produce the output in row bands (chunking); the bytes of every
  * band equal those of the whole-image call.
  *
  * Layout: NHWC (channels last), bfloat16 activations and weights, fp32
  * accumulation, one bf16 rounding of each output.  The summed weights are
- * rounded to bf16 once (xema_vae_upconv_prepare); that rounding, and the
- * output rounding, are the only departures from the exact definition.
+ * formed in fp32 and split into hi = bf16(sum) and lo = bf16(sum - hi)
+ * (xema_vae_upconv_prepare), which carry each to about 2^-17 of its size,
+ * so the output rounding is the only departure from the exact definition
+ * beyond fp32 accumulation.
  *
  * Conventions of xema.h apply: status codes, validation before any launch,
  * no device allocation, asynchronous on `stream`, 16-byte device pointers.
@@ -40,8 +43,8 @@
 extern "C" {
 #endif
 
-/* Bytes of the phase-summed weights: 4 phases x co x 4 taps x ci bf16
- * (32 ci co).  Errors: INVALID_ARG for NULL or non-positive sizes;
+/* Bytes of the phase-summed weights: 4 phases x co x 8 (4 taps, hi then
+ * lo) x ci bf16 (64 ci co).  Errors: INVALID_ARG for NULL or non-positive sizes;
  * UNSUPPORTED unless ci is a multiple of 64 and co a multiple of 256.      */
 XEMA_API int xema_vae_upconv_weight_bytes(int32_t ci, int32_t co, int64_t* bytes);
 
@@ -49,10 +52,11 @@ XEMA_API int xema_vae_upconv_weight_bytes(int32_t ci, int32_t co, int64_t* bytes
  *   w    device, bf16 [co, 3, 3, ci] (OHWI), read only
  *   wp   device, xema_vae_upconv_weight_bytes bytes, written; must not
  *        overlap w
- * wp[p][o][t][c] (p = 2 py + px the output phase, t = 2 a + b the source
- * offset) sums w[o][ky][kx][c] over the kernel rows ky landing on source row
- * offset a ({0} | {1, 2} when py = 0, {0, 1} | {2} when py = 1) and the
- * columns kx landing on b (the same with px), in fp32, rounded to bf16.
+ * With s = the fp32 sum of w[o][ky][kx][c] over the kernel rows ky landing
+ * on source row offset a ({0} | {1, 2} when py = 0, {0, 1} | {2} when
+ * py = 1) and the columns kx landing on b (the same with px), for output
+ * phase p = 2 py + px and source offset t = 2 a + b: wp[p][o][t][c] =
+ * bf16(s) and wp[p][o][4 + t][c] = bf16(s - bf16(s)), round to nearest even.
  * Errors: as xema_vae_upconv_weight_bytes; MISALIGNED.                    */
 XEMA_API int xema_vae_upconv_prepare(const void* w, int32_t ci, int32_t co, void* wp, void* stream);
 

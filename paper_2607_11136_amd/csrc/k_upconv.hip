@@ -13,21 +13,27 @@
 // same source pixel:
 //   source offset a = 0, 1 takes kernel rows {0} and {1, 2} when py = 0,
 //   and {0, 1} and {2} when py = 1 (the same for columns with px).
-// That is 16 C_in C_out multiply-adds per input pixel instead of the 36 of
-// the convolution over the upsampled image.  k_upconv_prep forms the summed
-// weights once per layer (fp32 sums, one bf16 rounding).
+// k_upconv_prep forms the summed weights once per layer as fp32 sums and
+// keeps each as a pair of bf16 values, hi = the sum rounded to bf16 and lo =
+// the remainder rounded to bf16, which together carry it to about 2^-17 of
+// its size: both are applied, so no rounding of the weights departs from the
+// definition beyond fp32 accumulation.  That is 32 C_in C_out multiply-adds
+// per input pixel (four phases, four taps, hi and lo) against the 36 of the
+// convolution over the upsampled image.
 //
 // Each phase is an implicit GEMM: M = the phase's output pixels, N = C_out,
-// K = 4 taps x C_in, with the A rows gathered from the input by tap.  Tiling
+// K = 8 x C_in (the four taps with their hi weights, then the four taps with
+// their lo weights), with the A rows gathered from the input by tap.  Tiling
 // and pipeline follow k_gemm: 256 x 256 tiles, K steps of 64 channels of one
 // tap, two LDS stages filled by buffer_load ... lds, eight waves of 32x32x16
 // MFMAs.  A tap that falls outside the image (or a row past M) is issued at an
 // offset with bit 31 set, beyond the buffer's range, so it reads zeros.  The
 // four phases of a tile run next to each other on one XCD and share its L2.
 //
-// Determinism: every output element sums its taps in a fixed order (tap-major,
-// channels ascending, one MFMA per 16 channels), whatever rows a call covers,
-// so a stage computed in row bands equals the stage computed at once.
+// Determinism: every output element sums its taps in a fixed order (the hi
+// taps, then the lo taps, tap-major, channels ascending, one MFMA per 16
+// channels), whatever rows a call covers, so a stage computed in row bands
+// equals the stage computed at once.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -66,9 +72,11 @@ __device__ __forceinline__ void barrier_all() {
 
 }  // namespace
 
-// wp[p][o][t][c] = sum of w[o][ky][kx][c] over the kernel taps (ky, kx) of
-// phase p = 2 py + px that land on source offset t = 2 a + b; fp32 sums in
-// ascending (ky, kx), rounded once to bf16.
+// The phase-summed weights: s = the sum of w[o][ky][kx][c] over the kernel
+// taps (ky, kx) of phase p = 2 py + px that land on source offset t = 2 a +
+// b, in fp32 in ascending (ky, kx); wp[p][o][t][c] = hi = bf16(s) and
+// wp[p][o][4 + t][c] = bf16(s - hi) (s - hi is exact in fp32).  One thread
+// per (p, o, t, c) writes both.
 __global__ void k_upconv_prep(const uint16_t* __restrict__ w, int ci, int co, uint16_t* __restrict__ wp) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t total = (int64_t)16 * co * ci;
@@ -86,7 +94,11 @@ __global__ void k_upconv_prep(const uint16_t* __restrict__ w, int ci, int co, ui
   float s = 0.f;
   for (int ky = r0; ky <= r1; ++ky)
     for (int kx = c0; kx <= c1; ++kx) s += bf16_bits_to_f32(w[(((int64_t)o * 3 + ky) * 3 + kx) * ci + c]);
-  wp[idx] = __builtin_bit_cast(uint16_t, (bf16)s);
+  const bf16 hi = (bf16)s;
+  const bf16 lo = (bf16)(s - (float)hi);
+  uint16_t* row = wp + (((int64_t)p * co + o) * 8) * ci;
+  row[(int64_t)t * ci + c] = __builtin_bit_cast(uint16_t, hi);
+  row[(int64_t)(4 + t) * ci + c] = __builtin_bit_cast(uint16_t, lo);
 }
 
 __global__ __launch_bounds__(UNWAVES * 64, 1) void k_upconv(UpconvParams p) {
@@ -94,7 +106,7 @@ __global__ __launch_bounds__(UNWAVES * 64, 1) void k_upconv(UpconvParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2][UA_BYTES + UB_BYTES];
 
   const int ci = p.ci, co = p.co, W = p.w, H = p.h;
-  const int KT = 4 * ci / UBK;             // K steps: 4 taps x ci / 64
+  const int KT = 8 * ci / UBK;             // K steps: (4 hi + 4 lo taps) x ci / 64
   const int cpt = ci / UBK;                // K steps per tap
   const int64_t M = (int64_t)p.n * p.row_count * W;   // output pixels of one phase
   const int tiles_m = (int)((M + UBM - 1) / UBM);
@@ -121,8 +133,8 @@ __global__ __launch_bounds__(UNWAVES * 64, 1) void k_upconv(UpconvParams p) {
   const int wm = wave / (UBN / UWN), wn = wave % (UBN / UWN);
 
   const __amdgpu_buffer_rsrc_t ra = rsrc(p.x, (int64_t)p.n * H * W * ci * 2);
-  const uint16_t* wph = p.wp + ((int64_t)phase * co + n0) * 4 * ci;
-  const __amdgpu_buffer_rsrc_t rb = rsrc(wph, (int64_t)UBN * 4 * ci * 2);
+  const uint16_t* wph = p.wp + ((int64_t)phase * co + n0) * 8 * ci;
+  const __amdgpu_buffer_rsrc_t rb = rsrc(wph, (int64_t)UBN * 8 * ci * 2);
 
   // A rows: load c of this wave fills tile rows (wave*UA_LOADS + c)*URPL +
   // lane/USLOTS; each row is one output pixel (frame f, source row i, column
@@ -153,16 +165,18 @@ __global__ __launch_bounds__(UNWAVES * 64, 1) void k_upconv(UpconvParams p) {
 #pragma unroll
   for (int c = 0; c < UB_LOADS; ++c) {
     const int row = (wave * UB_LOADS + c) * URPL + lane / USLOTS;
-    b_off[c] = (uint32_t)(row * 4 * ci * 2 + ((lane % USLOTS) ^ swz(row)) * 16);
+    b_off[c] = (uint32_t)(row * 8 * ci * 2 + ((lane % USLOTS) ^ swz(row)) * 16);
   }
 
   auto issue = [&](int kt, int idx) {
     uint8_t* st = smem[kt & 1];
     if (idx < UA_LOADS) {
-      const int tap = kt / cpt;                       // >= 4 past the last step
+      const int tap = kt / cpt;                       // 0-3 hi, 4-7 lo, >= 8 past the last step
+      const int src = tap & 3;                        // the source offset both weights apply to
       const uint32_t cbyte = (uint32_t)((kt - tap * cpt) * UBK * 2);
-      const uint32_t tdelta = (uint32_t)((((tap >> 1) * W) + (tap & 1)) * ci * 2);
-      const uint32_t oob = (((a_valid[idx] >> tap) & 1u) ^ 1u) << 31;
+      const uint32_t tdelta = (uint32_t)((((src >> 1) * W) + (src & 1)) * ci * 2);
+      const uint32_t valid = tap < 8 ? (a_valid[idx] >> src) & 1u : 0u;
+      const uint32_t oob = (valid ^ 1u) << 31;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (wave * UA_LOADS + idx) * 1024), 16,
                                                (a_base[idx] + tdelta + cbyte) | oob, 0, 0, 0);
     } else {

@@ -18,7 +18,7 @@ bool overlaps(const void* a, int64_t an, const void* b, int64_t bn) {
 int check_channels(int32_t ci, int32_t co) {
   if (ci <= 0 || co <= 0) return XEMA_ERR_INVALID_ARG;
   if (ci % 64 || co % 256) return XEMA_ERR_UNSUPPORTED;
-  if ((int64_t)32 * ci * co >= ((int64_t)1 << 31)) return XEMA_ERR_UNSUPPORTED;
+  if ((int64_t)64 * ci * co >= ((int64_t)1 << 31)) return XEMA_ERR_UNSUPPORTED;
   return XEMA_OK;
 }
 
@@ -28,7 +28,7 @@ extern "C" int xema_vae_upconv_weight_bytes(int32_t ci, int32_t co, int64_t* byt
   if (!bytes) return XEMA_ERR_INVALID_ARG;
   const int st = check_channels(ci, co);
   if (st != XEMA_OK) return st;
-  *bytes = (int64_t)32 * ci * co;
+  *bytes = (int64_t)64 * ci * co;
   return XEMA_OK;
 }
 
@@ -37,7 +37,7 @@ extern "C" int xema_vae_upconv_prepare(const void* w, int32_t ci, int32_t co, vo
   const int st = check_channels(ci, co);
   if (st != XEMA_OK) return st;
   if (!aligned(w, 16) || !aligned(wp, 16)) return XEMA_ERR_MISALIGNED;
-  if (overlaps(w, (int64_t)18 * ci * co, wp, (int64_t)32 * ci * co)) return XEMA_ERR_INVALID_ARG;
+  if (overlaps(w, (int64_t)18 * ci * co, wp, (int64_t)64 * ci * co)) return XEMA_ERR_INVALID_ARG;
   return launch_upconv_prep((const uint16_t*)w, ci, co, (uint16_t*)wp, (hipStream_t)stream) ==
                  hipSuccess
              ? XEMA_OK
@@ -57,7 +57,7 @@ extern "C" int xema_vae_upconv(const void* x, int32_t n, int32_t h, int32_t w, i
   if ((int64_t)n * h * w > ((int64_t)1 << 30)) return XEMA_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(wp, 16) || !aligned(bias, 16) || !aligned(y, 16))
     return XEMA_ERR_MISALIGNED;
-  if (overlaps(y, y_bytes, x, x_bytes) || overlaps(y, y_bytes, wp, (int64_t)32 * ci * co) ||
+  if (overlaps(y, y_bytes, x, x_bytes) || overlaps(y, y_bytes, wp, (int64_t)64 * ci * co) ||
       overlaps(y, y_bytes, bias, (int64_t)co * 2))
     return XEMA_ERR_INVALID_ARG;
   UpconvParams p;

@@ -62,7 +62,7 @@ def test_summed_weights_byte_exact():
     st = Stage(s)
     w = W.bf16_bits_to_f64(st.inp.weight).astype(np.float32)      # [co, 3, 3, ci]
     rows = {0: [[0], [1, 2]], 1: [[0, 1], [2]]}
-    want = np.empty((4, s.co, 4, s.ci), dtype=np.float64)
+    want = np.empty((4, s.co, 8, s.ci), dtype=np.float64)
     for p in range(4):
         py, px = p >> 1, p & 1
         for t in range(4):
@@ -71,8 +71,10 @@ def test_summed_weights_byte_exact():
             for ky in rows[py][a]:
                 for kx in rows[px][b]:
                     acc = acc + w[:, ky, kx, :]
-            want[p, :, t, :] = _bf16_rne(acc)
-    got = st.wp.float().cpu().numpy().astype(np.float64).reshape(4, s.co, 4, s.ci)
+            hi = _bf16_rne(acc)
+            want[p, :, t, :] = hi
+            want[p, :, 4 + t, :] = _bf16_rne(acc - hi.astype(np.float32))   # the remainder is exact in fp32
+    got = st.wp.float().cpu().numpy().astype(np.float64).reshape(4, s.co, 8, s.ci)
     assert np.array_equal(got, want)
 
 
