@@ -17,17 +17,17 @@ pytestmark = pytest.mark.gpu
 
 
 def assert_vae_parity(got: np.ndarray, ref: np.ndarray, what: str):
-    """The bar, from the arithmetic.  Two bf16 roundings separate the GPU from
-    the exact definition: the output's own (its mean cost is the 'bf16 floor'
-    MAE(bf16_RNE(ref), ref)) and the one of each phase-summed weight, a
-    relative 2^-9 at most per weight, which moves an output by about as much
-    as its own rounding.  So MAE <= 2 floor + 1e-4 (fp32 accumulation), and
-    |g - o| <= 2e-2 max(|o|, 1) elementwise."""
+    """The bar, from the arithmetic (reading R26).  One bf16 rounding
+    separates the GPU from the exact definition: the output's own, whose mean
+    cost is the 'bf16 floor' MAE(bf16_RNE(ref), ref).  The phase-summed
+    weights enter as hi + lo bf16 pairs (about 2^-17 of each weight) and the
+    products accumulate in fp32, so MAE <= floor + 4e-4, and |g - o| <= 2e-2
+    max(|o|, 1) elementwise."""
     e = errors(got, ref)
     floor = float(np.mean(np.abs(W.bf16_bits_to_f64(W.to_bf16_bits(ref.astype(np.float32))) - ref)))
     print(f"{what}: {e} bf16 floor {floor:.3g}", flush=True)
     assert np.all(np.isfinite(got)), what
-    assert e["max_rel"] <= 2e-2 and e["mae"] <= 2 * floor + 1e-4, (what, e, floor)
+    assert e["max_rel"] <= 2e-2 and e["mae"] <= floor + 4e-4, (what, e, floor)
 
 SMALL = {
     "tiny": W.VAE_TINY,
