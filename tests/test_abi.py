@@ -239,7 +239,8 @@ def test_dual_stream_validation():
 def test_vae_upconv_validation():
     lib = X.lib()
     n = ctypes.c_int64()
-    assert lib.xema_vae_upconv_weight_bytes(256, 512, ctypes.byref(n)) == X.XEMA_OK and n.value == 32 * 256 * 512
+    # 4 phases x co x 8 (hi and lo of 4 taps) x ci bf16
+    assert lib.xema_vae_upconv_weight_bytes(256, 512, ctypes.byref(n)) == X.XEMA_OK and n.value == 64 * 256 * 512
     assert lib.xema_vae_upconv_weight_bytes(96, 256, ctypes.byref(n)) == X.XEMA_ERR_UNSUPPORTED
     assert lib.xema_vae_upconv_weight_bytes(64, 128, ctypes.byref(n)) == X.XEMA_ERR_UNSUPPORTED
     assert lib.xema_vae_upconv_weight_bytes(0, 256, ctypes.byref(n)) == X.XEMA_ERR_INVALID_ARG
