@@ -157,7 +157,14 @@ def bench_step(args, shape):
                       shape.rope_dims, shape.rope_theta, shape.ln_eps, shape.qk_eps,
                       shape.modulation_streams)
     req = X.request(shape.batch, shape.text_len, *shape.grid)
-    if args.weight_budget is not None:
+    step_plan = None
+    if args.device_budget is not None:
+        # offloading, serialization and chunking chosen together under one
+        # device budget (resident weights + the step's workspace)
+        costs = X.step_costs(args.h2d_gbps, args.block_tflops)
+        step_plan = X.xema_step_plan_budget(cfg, req, n, args.staging, args.device_budget, costs)
+        plan = step_plan.offload
+    elif args.weight_budget is not None:
         plan = X.xema_offload_plan_budget(cfg, n, args.weight_budget, args.staging)
     else:
         plan = X.xema_offload_plan_k(cfg, n, args.offload, args.staging)
@@ -185,7 +192,7 @@ def bench_step(args, shape):
         blocks.append(X.block_weights(w))
     x = rand((shape.batch, shape.seq_len, shape.hidden), 1.0)
     cond = rand((shape.batch, shape.cond_dim), 1.0)
-    nbytes = X.xema_step_workspace_bytes(cfg, req, 0, plan)
+    nbytes = step_plan.workspace_bytes if step_plan else X.xema_step_workspace_bytes(cfg, req, 0, plan)
     ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     out = torch.empty((shape.batch, shape.seq_len, shape.hidden), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -194,7 +201,10 @@ def bench_step(args, shape):
     torch.cuda.reset_peak_memory_stats()
 
     def step():
-        X.xema_dit_step_fwd(cfg, req, x, blocks, plan, cond, 0, ws, nbytes, out, stream, copy_stream)
+        if step_plan:
+            X.xema_dit_step_fwd_planned(cfg, req, x, blocks, step_plan, cond, ws, nbytes, out, stream, copy_stream)
+        else:
+            X.xema_dit_step_fwd(cfg, req, x, blocks, plan, cond, 0, ws, nbytes, out, stream, copy_stream)
 
     for _ in range(args.warmup):
         step()
@@ -241,8 +251,13 @@ def bench_step(args, shape):
             "h2d_bytes_per_step": plan.n_offloaded * plan.block_weight_bytes,
             "h2d_block_GBps": None if h2d_gbs is None else round(h2d_gbs, 1),
             "device_peak_bytes": int(torch.cuda.max_memory_allocated()),
+            "workspace_bytes": nbytes,
         },
     }
+    if step_plan:
+        result["config"].update({"device_budget_bytes": args.device_budget, "batch_group": step_plan.batch_group,
+                                 "chunk_tokens": step_plan.chunk_tokens, "device_bytes": step_plan.device_bytes,
+                                 "est_ms": round(step_plan.est_ms, 3)})
     print(json.dumps(result), flush=True)
 
 
@@ -440,6 +455,11 @@ def main():
     ap.add_argument("--weight-budget", type=int, default=None,
                     help="device weight budget in bytes; the plan picks the smallest K (step mode)")
     ap.add_argument("--staging", type=int, default=2, help="device staging slots (step mode)")
+    ap.add_argument("--device-budget", type=int, default=None,
+                    help="one device budget for resident weights and the step's workspace: the plan picks "
+                         "offloading, batch groups and chunking together (step mode)")
+    ap.add_argument("--h2d-gbps", type=float, default=56.0, help="copy rate the step plan's model assumes")
+    ap.add_argument("--block-tflops", type=float, default=1000.0, help="block rate the step plan's model assumes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--bf16-weights", action="store_true",
                     help="hand W_o, W_up, W_down over in bf16 (converted into the arena on every call) "

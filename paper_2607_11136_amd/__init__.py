@@ -115,6 +115,15 @@ class OffloadPlan(ctypes.Structure):
         return [i for i in range(self.n_blocks) if self.offloaded[i]]
 
 
+class StepCosts(ctypes.Structure):
+    _fields_ = [("h2d_gbytes_per_s", ctypes.c_double), ("block_tflops", ctypes.c_double)]
+
+
+class StepPlan(ctypes.Structure):
+    _fields_ = [("offload", OffloadPlan), ("batch_group", ctypes.c_int32), ("chunk_tokens", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64), ("est_ms", ctypes.c_double)]
+
+
 _P = ctypes.c_void_p
 _I32, _I64, _F32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
 _SIGNATURES = {
@@ -153,6 +162,13 @@ _SIGNATURES = {
     "xema_dit_step_fwd": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
                                          ctypes.POINTER(BlockWeights), ctypes.POINTER(OffloadPlan),
                                          _P, _I32, _P, _I64, _P, _P, _P]),
+    "xema_step_plan_fixed": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _I32, _I32, _I32,
+                                            _I32, _I32, ctypes.POINTER(StepCosts), ctypes.POINTER(StepPlan)]),
+    "xema_step_plan_budget": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _I32, _I32, _I64,
+                                             ctypes.POINTER(StepCosts), ctypes.POINTER(StepPlan)]),
+    "xema_dit_step_fwd_planned": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
+                                                 ctypes.POINTER(BlockWeights), ctypes.POINTER(StepPlan), _P, _P,
+                                                 _I64, _P, _P, _P]),
     "xema_dit_block_fwd_pipelined": (ctypes.c_int, [ctypes.POINTER(BlockCfg), ctypes.POINTER(Request), _P,
                                                     ctypes.POINTER(BlockWeights), _P, _I32, _I32, _P, _I64, _P,
                                                     _P, _P]),
@@ -454,6 +470,47 @@ def xema_dit_step_fwd(cfg: BlockCfg, req: Request, tokens, weights: Sequence[Blo
                                    ctypes.byref(plan), _ptr(cond), chunk_tokens, _ptr(workspace),
                                    int(workspace_bytes), _ptr(out), _stream(stream), cs),
            "xema_dit_step_fwd")
+
+
+def step_costs(h2d_gbytes_per_s: float = 56.0, block_tflops: float = 1000.0) -> StepCosts:
+    """The latency model's rates (defaults: one MI355X, measured)."""
+    k = StepCosts()
+    k.h2d_gbytes_per_s, k.block_tflops = h2d_gbytes_per_s, block_tflops
+    return k
+
+
+def xema_step_plan_fixed(cfg: BlockCfg, req: Request, n_blocks: int, n_offloaded: int, n_staging: int,
+                         batch_group: int, chunk_tokens: int, costs: Optional[StepCosts] = None) -> StepPlan:
+    p = StepPlan()
+    _check(lib().xema_step_plan_fixed(ctypes.byref(cfg), ctypes.byref(req), n_blocks, n_offloaded, n_staging,
+                                      batch_group, chunk_tokens, ctypes.byref(costs or step_costs()),
+                                      ctypes.byref(p)), "xema_step_plan_fixed")
+    return p
+
+
+def xema_step_plan_budget(cfg: BlockCfg, req: Request, n_blocks: int, n_staging: int, device_budget_bytes: int,
+                          costs: Optional[StepCosts] = None) -> StepPlan:
+    """Raises XemaError (XEMA_ERR_BUDGET_TOO_SMALL, the plan with the least
+    device_bytes as `.plan`) when nothing fits."""
+    p = StepPlan()
+    st = lib().xema_step_plan_budget(ctypes.byref(cfg), ctypes.byref(req), n_blocks, n_staging,
+                                     int(device_budget_bytes), ctypes.byref(costs or step_costs()), ctypes.byref(p))
+    if st != XEMA_OK:
+        e = XemaError(st, "xema_step_plan_budget")
+        e.plan = p
+        raise e
+    return p
+
+
+def xema_dit_step_fwd_planned(cfg: BlockCfg, req: Request, tokens, weights: Sequence[BlockWeights],
+                              plan: StepPlan, cond, workspace, workspace_bytes: int, out, stream=None,
+                              copy_stream=None) -> None:
+    arr = (BlockWeights * len(weights))(*weights)
+    cs = None if copy_stream is None else (copy_stream if isinstance(copy_stream, int)
+                                           else copy_stream.cuda_stream)
+    _check(lib().xema_dit_step_fwd_planned(ctypes.byref(cfg), ctypes.byref(req), _ptr(tokens), arr,
+                                           ctypes.byref(plan), _ptr(cond), _ptr(workspace), int(workspace_bytes),
+                                           _ptr(out), _stream(stream), cs), "xema_dit_step_fwd_planned")
 
 
 # -- the VAE decoder's fused upsampling stage (include/xema_vae.h) -------------------------------

@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
 SOURCES = ["plan.cpp", "k_elementwise.hip", "k_gemm.hip", "k_attention.hip", "block.hip", "step.hip",
-           "k_upconv.hip", "vae.hip", "static_arena.hip"]
+           "k_upconv.hip", "vae.hip", "static_arena.hip",
+           "step_plan.cpp"]
 
 # Packed fp32 VALU forms are kept out of the generated code.
 HIPCC_FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-I" + INCLUDE,

@@ -221,7 +221,7 @@ namespace xema {
 // ch, out is [B, L, D] fp32.
 int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens, int x_dtype,
               const xema_block_weights& w, const void* cond, int64_t ch, uint8_t* ws,
-              const xema_plan& plan, float* out, hipStream_t s, hipStream_t aux) {
+              const xema_plan& plan, float* out, hipStream_t s, hipStream_t aux, bool clear_status) {
   const int64_t B = r.batch, L = seq_len(r), D = c.hidden, F = c.mlp_hidden, Dc = c.cond_dim;
   const int64_t Lp = padded_len(L);
   auto slot = [&](int id) { return (void*)(ws + plan.slot_offset[id]); };
@@ -254,9 +254,10 @@ int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens
   const int64_t txt_delta = dual_stream(c) ? B * 6 * D : 0;
   auto sel_at = [&](int64_t t0) { return ModSel{t0, r.text_len, txt_delta}; };
 
-  // step 0 (the first launch also clears the range flags)
+  // step 0 (the first launch of a call also clears the range flags)
   XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_w,
-                        (const uint16_t*)w.ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s, status));
+                        (const uint16_t*)w.ada_b, (int)B, (int)Dc, (int)(6 * D), mod, s,
+                        clear_status ? status : nullptr));
   if (dual_stream(c))
     XEMA_TRY(launch_adaln((const uint16_t*)cond, (const uint16_t*)w.ada_txt_w,
                           (const uint16_t*)w.ada_txt_b, (int)B, (int)Dc, (int)(6 * D),
@@ -443,7 +444,7 @@ int xema::block_fwd(const xema_block_cfg* cfg, const xema_request* req, const vo
     const bool last = b0 + g >= B;
     st = run_block(c, last ? rl : rg, (const uint16_t*)tokens + b0 * L * D, XEMA_BF16, *w,
                    (const uint16_t*)cond + b0 * Dc, ch, (uint8_t*)workspace, last ? plan_l : plan_g,
-                   (float*)out + b0 * L * D, (hipStream_t)stream, (hipStream_t)aux_stream);
+                   (float*)out + b0 * L * D, (hipStream_t)stream, (hipStream_t)aux_stream, b0 == 0);
     if (st != XEMA_OK) return st;
   }
   return XEMA_OK;

@@ -9,39 +9,38 @@
 
 namespace xema {
 
-namespace {
-
-struct Rect {
-  int id;
-  int64_t size;   // bytes, already rounded to kAlign
-  int begin, end; // half-open step lifetime
-};
-
-bool lifetimes_overlap(const Rect& a, const Rect& b) {
-  return a.begin < b.end && b.begin < a.end;
-}
-
 // Algorithm 1: largest tensor first (ties: earlier lifetime start, then id);
 // each tensor goes to the bottom of the smallest gap, among the holes left by
 // already-placed tensors with overlapping lifetimes, that can hold it (ties:
-// lower address); with no such gap it goes right above those tensors.
-int64_t pack(const std::vector<Rect>& rects, std::vector<int64_t>* offsets) {
+// lower address); with no such gap it goes right above those tensors.  The
+// placed tensors alive at each step are kept in per-step lists, so the
+// tensors whose lifetimes overlap the next one are found without scanning
+// every placed tensor (the set, and so the placement, is the same).
+int64_t static_layout(const std::vector<LayoutRect>& rects, std::vector<int64_t>* offsets) {
   const size_t n = rects.size();
   std::vector<size_t> order(n);
-  for (size_t i = 0; i < n; ++i) order[i] = i;
+  int horizon = 0;
+  for (size_t i = 0; i < n; ++i) {
+    order[i] = i;
+    horizon = std::max(horizon, rects[i].end);
+  }
   std::sort(order.begin(), order.end(), [&](size_t x, size_t y) {
     if (rects[x].size != rects[y].size) return rects[x].size > rects[y].size;
     if (rects[x].begin != rects[y].begin) return rects[x].begin < rects[y].begin;
     return rects[x].id < rects[y].id;
   });
   offsets->assign(n, -1);
-  std::vector<size_t> placed;
+  std::vector<std::vector<size_t>> alive((size_t)std::max(horizon, 0));
+  std::vector<size_t> seen(n, (size_t)-1);
   std::vector<std::pair<int64_t, int64_t>> busy;
   for (size_t i : order) {
     busy.clear();
-    for (size_t j : placed)
-      if (lifetimes_overlap(rects[i], rects[j]))
-        busy.emplace_back((*offsets)[j], (*offsets)[j] + rects[j].size);
+    for (int t = std::max(rects[i].begin, 0); t < rects[i].end; ++t)
+      for (size_t j : alive[(size_t)t])
+        if (seen[j] != i) {
+          seen[j] = i;
+          busy.emplace_back((*offsets)[j], (*offsets)[j] + rects[j].size);
+        }
     std::sort(busy.begin(), busy.end());
     int64_t cursor = 0, top = 0;
     int64_t best_addr = -1, best_len = 0;
@@ -57,12 +56,14 @@ int64_t pack(const std::vector<Rect>& rects, std::vector<int64_t>* offsets) {
       top = std::max(top, iv.second);
     }
     (*offsets)[i] = best_addr >= 0 ? best_addr : top;
-    placed.push_back(i);
+    for (int t = std::max(rects[i].begin, 0); t < rects[i].end; ++t) alive[(size_t)t].push_back(i);
   }
   int64_t peak = 0;
   for (size_t i = 0; i < n; ++i) peak = std::max(peak, (*offsets)[i] + rects[i].size);
   return peak;
 }
+
+namespace {
 
 int64_t rope_table_bytes(const xema_block_cfg& cfg, const xema_request& req) {
   const int64_t g[3] = {req.grid_t, req.grid_h, req.grid_w};
@@ -137,11 +138,11 @@ int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t
       {2 * B * c * F, 8, 10},                      // XEMA_SLOT_HID
       {4 * XEMA_STATUS_WORDS, 0, 10},              // XEMA_SLOT_STATUS
   };
-  std::vector<Rect> rects;
+  std::vector<LayoutRect> rects;
   for (int i = 0; i < XEMA_NUM_SLOTS; ++i)
     rects.push_back({i, round_up(spec[i].bytes, kAlign), spec[i].begin, spec[i].end});
   std::vector<int64_t> offsets;
-  const int64_t peak = pack(rects, &offsets);
+  const int64_t peak = static_layout(rects, &offsets);
   std::memset(out, 0, sizeof(*out));
   out->chunk_tokens = (int32_t)c;
   out->n_slots = XEMA_NUM_SLOTS;

@@ -3,9 +3,11 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <vector>
 
 #include "xema.h"
 #include "xema_ops.h"
+#include "xema_step.h"
 
 namespace xema {
 
@@ -26,6 +28,18 @@ inline int64_t effective_chunk(int64_t L, int64_t chunk) {
   return (chunk <= 0 || chunk >= L) ? L : chunk;
 }
 
+// A tensor of a static layout: `size` bytes (already rounded to kAlign),
+// alive over the half-open step range [begin, end).
+struct LayoutRect {
+  int id;
+  int64_t size;
+  int begin, end;
+};
+
+// Algorithm 1 (Sec. 6.1) over `rects`: offsets in input order; returns the
+// peak address.
+int64_t static_layout(const std::vector<LayoutRect>& rects, std::vector<int64_t>* offsets);
+
 // Fill `out` with the slot table at chunk `c` and its Algorithm 1 offsets.
 int layout_for_chunk(const xema_block_cfg& cfg, const xema_request& req, int64_t c,
                      xema_plan* out);
@@ -39,6 +53,36 @@ void block_weight_sizes(const xema_block_cfg& cfg, int64_t bytes[kWeightTensors]
 inline const void* const* weight_ptrs(const xema_block_weights& w) { return &w.ada_w; }
 inline const void** weight_ptrs(xema_block_weights& w) { return &w.ada_w; }
 static_assert(sizeof(xema_block_weights) == kWeightTensors * sizeof(void*), "weight struct layout");
+
+// -- the N-block step (step_plan.cpp) --
+
+// Offsets of a block's tensors packed in a staging slot (a tensor the block
+// does not use takes no space); returns the slot size.
+int64_t packed_offsets(const xema_block_cfg& c, int64_t off[kWeightTensors]);
+// The block hyper-parameters alone (a one-token request stands in).
+int validate_cfg(const xema_block_cfg* cfg);
+// The offload plan with K = k of n blocks (blocks floor((j+1) n / k) - 1).
+void fill_offload_plan(const xema_block_cfg& c, int n, int k, int staging, xema_offload_plan* out);
+// XEMA_OK when `plan` is the plan fill_offload_plan makes for this cfg.
+int check_offload_plan(const xema_block_cfg& c, const xema_offload_plan* plan);
+
+// The step's static layout (Algorithm 1 over its lifetime trace): the
+// block's slot table for a group-sequence request at the chunk, the offset
+// of every block's every slot, of each residual buffer the workspace holds
+// (block i's output; -1 where the caller's out holds it) and of each staging
+// slot, and the peak.
+struct StepLayout {
+  xema_plan block;
+  std::vector<int64_t> slot_off;     // [n_blocks * XEMA_NUM_SLOTS]
+  std::vector<int64_t> resid_off;    // [n_blocks]
+  std::vector<int64_t> staging_off;  // [n_staging]
+  int64_t peak = 0;
+};
+int step_layout(const xema_block_cfg& c, const xema_request& r, int n_blocks, int group, int64_t chunk,
+                int n_staging, int64_t slot_bytes, StepLayout* out);
+// xema_step_plan_fixed without the argument checks.
+int make_step_plan(const xema_block_cfg& c, const xema_request& r, int n_blocks, int n_offloaded, int n_staging,
+                   int group, int64_t chunk, const xema_step_costs& costs, xema_step_plan* out);
 
 // The block forward behind every xema_dit_block_fwd* entry point: validates
 // the call (the workspace must hold the layout of a batch_group-sequence
@@ -61,10 +105,13 @@ namespace xema {
 // [B, L, D] in x_dtype (XEMA_BF16 or XEMA_F32), the arena follows `plan`,
 // out is [B, L, D] fp32.  With a second stream `aux` (not null, not s) and
 // two chunks or more, each chunk's attention runs on aux, overlapping the
-// previous chunk's projections; the output is the same.
+// previous chunk's projections; the output is the same.  clear_status:
+// whether this run starts the range flags from zero (the first run of a
+// call; later groups and blocks of the call add to them).
 int run_block(const xema_block_cfg& c, const xema_request& r, const void* tokens, int x_dtype,
               const xema_block_weights& w, const void* cond, int64_t ch, uint8_t* ws,
-              const xema_plan& plan, float* out, hipStream_t s, hipStream_t aux = nullptr);
+              const xema_plan& plan, float* out, hipStream_t s, hipStream_t aux = nullptr,
+              bool clear_status = true);
 }  // namespace xema
 #endif
 

@@ -35,7 +35,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = X.lib()
     declared = _declared_symbols()
-    assert len(declared) == 25, declared
+    assert len(declared) == 28, declared
     for name in declared:
         assert hasattr(lib, name), name
     assert declared == set(X.EXPORTED)

@@ -129,3 +129,23 @@ def test_out_of_range_intermediate_raises_its_flag(kind, bit):
     clean = Device(W.make_inputs(D64))
     out, ws2, plan = clean.run(0, ws=ws)
     assert X.xema_block_status(plan, ws2) == 0
+
+
+def test_range_flags_cover_every_group_of_a_serialized_call():
+    """Only the first sequence's conditioning is huge (its modulation leaves
+    the fp16 range); run in groups of one sequence, the flag the first group
+    raises survives the second group."""
+    inp = W.make_inputs(D64)
+    cond = inp.cond.copy()
+    cond[0] = _scaled(cond[0], 1e6)
+    dev = Device(W.Inputs(D64, inp.x, cond, inp.weights))
+    sub = X.request(1, D64.text_len, *D64.grid)
+    plan = X.xema_workspace_layout(dev.cfg, sub, 0)
+    ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device="cuda:0")
+    out = torch.empty((D64.batch, D64.seq_len, D64.hidden), dtype=torch.float32, device="cuda:0")
+    X.xema_dit_block_fwd_serial(dev.cfg, dev.req, dev.x, dev.weights, dev.cond, 1, 0, ws, ws.numel(), out)
+    torch.cuda.synchronize()
+    flags = X.xema_block_status(plan, ws)
+    print(f"serialized call, first sequence out of range: flags {flags:#x}", flush=True)
+    assert flags != 0
+    assert torch.isfinite(out[1]).all()     # the second sequence is unaffected
