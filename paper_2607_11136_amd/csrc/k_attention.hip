@@ -23,13 +23,11 @@
 //     the row sum), two wave groups run offset by a phase over a 3-stage LDS
 //     ring so one group's softmax overlaps the other's MFMAs;
 //   k_attention_lazy (used at d = 64): two column blocks per wave (half the
-//     LDS reads per score) and a 2-stage ring.  The reference is subtracted
-//     by the MFMA: one more k-step multiplies a column of ones in the key
-//     operand by -mrow in the query operand (kept fp16-representable), which
-//     costs 4 MFMAs per tile instead of 64 subtractions per lane.  P is then
-//     taken straight from the MFMA output, and the trigger is the same P sum
-//     as above, so the common path has no max reduction; the rare rescaling
-//     path finds the tile max and recomputes P.  The two columns run offset
+//     LDS reads per score) and a 2-stage ring.  The reference max enters as
+//     the accumulator input of the first score MFMA as well, so P is taken
+//     straight from the MFMA output, and the trigger is the same P sum as
+//     above: the common path has no max reduction and no subtraction; the
+//     rare rescaling path finds the tile max and recomputes P.  The two columns run offset
 //     within a tile, so that MFMAs of one are issued beside the
 //     exponentials of the other.  Scores must stay below 2^16 in log2 units.
 // Measured on the workloads' own Q/K/V, each is the faster one at its width.
@@ -155,16 +153,15 @@ struct WaveState {
   f32x16 minit[QB];          // -mrow in all 16 entries
   float mrow[QB];            // reference max in use (log2 units)
   float lrow[QB];            // this lane's share of the row sum
-  f16x8 mneg[QB];            // B fragment of the extra k-step: -mrow at k = 0
 };
 
-// S^T - mrow for two 32-key blocks of one query column: the score MFMAs plus
-// one k-step of (a column of ones) x (-mrow), so the scores arrive shifted.
+// S^T - mrow for two 32-key blocks of one query column: -mrow is the
+// accumulator input of the first k-step, so the scores arrive shifted.
 // (The key fragments are the same for every column; the compiler reads them
 // from LDS once per tile.)
 template <int HD>
-__device__ __forceinline__ void scores_col(const uint8_t* Ks, const f16x8 (&qc)[HD / 16], f16x8 mneg,
-                                           f16x8 ones, int krow, int kswz, int hi, f32x16 (&s)[2]) {
+__device__ __forceinline__ void scores_col(const uint8_t* Ks, const f16x8 (&qc)[HD / 16], const f32x16& minit,
+                                           int krow, int kswz, int hi, f32x16 (&s)[2]) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int row = kb * 32 + krow;
@@ -172,9 +169,8 @@ __device__ __forceinline__ void scores_col(const uint8_t* Ks, const f16x8 (&qc)[
     for (int kk = 0; kk < HD / 16; ++kk) {
       const int slot16 = (kk * 2 + hi) ^ kswz;
       const f16x8 kf = *reinterpret_cast<const f16x8*>(Ks + row * (HD * 2) + slot16 * 16);
-      s[kb] = mma(kf, qc[kk], kk == 0 ? f32x16{} : s[kb]);
+      s[kb] = mma(kf, qc[kk], kk == 0 ? minit : s[kb]);
     }
-    s[kb] = mma(ones, mneg, s[kb]);
   }
 }
 
@@ -271,12 +267,12 @@ __device__ __forceinline__ void tile_softmax(const f32x16 (&s)[2][QB], bool firs
 }
 
 // Online softmax for k_attention_lazy.  The scores arrive as s - mrow (the
-// extra k-step of scores_col), so the common path packs P = 2^s straight
+// accumulator input of scores_col), so the common path packs P = 2^s straight
 // from the MFMA output; its sum (exp_pack) is the row sum.  A column grows when
 // the larger of its two lanes' sums exceeds PMAX (a P that overflows fp16
 // makes its sum infinite, so it always grows) and on the first tile; then
-// rescale_col moves mrow to the tile max, rounded to fp16 because it feeds
-// the MFMA, rescales O and the row sum, and recomputes P from the scores
+// rescale_col moves mrow to the tile max, rounded to fp16 so that the
+// shift (a difference of two such values) is exact in fp32, rescales O and the row sum, and recomputes P from the scores
 // shifted by the move.  Lanes whose column does not grow shift by 0 and
 // scale by 1.0, which reproduces their P bit for bit, so a query's result
 // never depends on the others of its wave.
@@ -303,9 +299,8 @@ __device__ __forceinline__ void rescale_col(const f32x16 (&s)[2], bool first, in
 #pragma unroll
     for (int r = 0; r < 16; ++r) st.oacc[c][d][r] *= alpha;
   lsp = exp_pack<true>(s[0], s[1], shift, pfc);   // x - 0 = x for the others
-  f16x8 mn = {};
-  mn[0] = hi ? (f16)0.f : (f16)(-st.mrow[c]);
-  st.mneg[c] = mn;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) st.minit[c][r] = -st.mrow[c];
 }
 
 // O^T += V^T P^T
@@ -507,13 +502,11 @@ __device__ __forceinline__ void lazy_iter(uint8_t (*smem)[2 * KV * HD * 2], int 
   const uint8_t* Ks = smem[stage];
   const uint8_t* Vs = smem[stage] + K_BYTES;
   const bool first = kv == 0;
-  f16x8 ones = {};
-  ones[0] = hi ? (f16)0.f : (f16)1.f;
   f32x16 s0[2], s1[2];
   f16x8 pf[QB][2][2];
-  scores_col<HD>(Ks, qf[0], st.mneg[0], ones, krow, kswz, hi, s0);
+  scores_col<HD>(Ks, qf[0], st.minit[0], krow, kswz, hi, s0);
   if (LAST && tail < KV) mask_tail_col(s0, tail, hi);
-  scores_col<HD>(Ks, qf[1], st.mneg[1], ones, krow, kswz, hi, s1);
+  scores_col<HD>(Ks, qf[1], st.minit[1], krow, kswz, hi, s1);
   float lsp0 = exp_pack<false>(s0[0], s0[1], 0.f, pf[0]);
   if (__builtin_amdgcn_ballot_w64(first || lsp0 > PMAX))
     rescale_col<HD, QB>(s0, first, 0, lsp0, st, pf[0], hi);
@@ -620,7 +613,6 @@ __global__ __launch_bounds__(NW * 64) void k_attention_lazy(AttnParams p) {
     st.lrow[c] = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) st.minit[c][r] = 0.f;
-    st.mneg[c] = f16x8{};
 #pragma unroll
     for (int d = 0; d < NDB; ++d)
 #pragma unroll
