@@ -658,12 +658,16 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, int64_t m_begin, 
 // second launch behind the first costs about 3072/K waves (its start-up and
 // the first launch's drain, measured at roughly 50 us).  E.g. 17776 x 3072 x
 // 12288: 840 tiles = 4 waves, or 768 + 132 half tiles = 3 + 0.62 + 0.25.
-// One launch, two tile heights: workgroups below tiles_big take 256-row
-// tiles of rows [0, split), the rest 128-row tiles of rows [split, M).  The
-// half-height tiles come last in dispatch order and fill the CUs the last
-// round of full tiles leaves idle.
+// One launch, two tile heights: 256-row tiles of rows [0, split) and
+// 128-row tiles of rows [split, M).  The first `first_small` workgroups take
+// half-height tiles, the next tiles_big the full tiles, the rest the other
+// half-height tiles, which come last in dispatch order and fill the CUs the
+// last round of full tiles leaves idle.  Half-height tiles first put the
+// CUs that run them about half a tile ahead of the others, so that their
+// epilogues do not all fall in the same interval.
 template <typename T, int EPI, typename CT, typename RT>
 __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t split, int tiles_big,
+                                                         int first_small,
                                                          const uint16_t* __restrict__ bias,
                                                          CT* __restrict__ cout,
                                                          const RT* __restrict__ resid,
@@ -672,11 +676,13 @@ __global__ __launch_bounds__(NWAVES * 64, 1) void k_gemm(GemmParams p, int64_t s
   constexpr int STAGES = NS * (256 * BK * 2 + B_BYTES);
   constexpr int EPI_LDS = EPI == EPI_QKV_HEADS_128 ? qkv_epi_lds_bytes(256, 128) : 0;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES > EPI_LDS ? STAGES : EPI_LDS];
-  if ((int)blockIdx.x < tiles_big)
-    gemm_tile<T, EPI, CT, RT, 256>(p, 0, split, (int)blockIdx.x, smem, bias, cout, resid, gate);
+  const int bx = (int)blockIdx.x;
+  if (bx < first_small)
+    gemm_tile<T, EPI, CT, RT, 128>(p, split, p.M, bx, smem, bias, cout, resid, gate);
+  else if (bx < first_small + tiles_big)
+    gemm_tile<T, EPI, CT, RT, 256>(p, 0, split, bx - first_small, smem, bias, cout, resid, gate);
   else
-    gemm_tile<T, EPI, CT, RT, 128>(p, split, p.M, (int)blockIdx.x - tiles_big, smem, bias, cout, resid,
-                                   gate);
+    gemm_tile<T, EPI, CT, RT, 128>(p, split, p.M, bx - tiles_big, smem, bias, cout, resid, gate);
 }
 
 // Completion time of n_big full tiles, then n_small half-height tiles costing
@@ -729,8 +735,17 @@ static hipError_t launch_t(const GemmParams& p, hipStream_t s) {
   const int64_t split = gemm_row_split(p.M, tiles_n);
   const int64_t big = ((split + 255) / 256) * tiles_n;
   const int64_t small = ((p.M - split + 127) / 128) * tiles_n;
+  // Up to 192 half-height tiles first (a multiple of 8, so that each set of
+  // tiles keeps its XCD-aware order) for the gated-residual epilogue at
+  // short K (the out-projection), whose epilogue is a large share of a tile.
+  // Measured against none first: 17776 x 3072 x 3072 5% faster, 18432 rows
+  // 3.5%, 106306 rows 2%, 57224 x 4096 x 4096 unchanged; at K = 12288 and
+  // with the other epilogues no faster.  The dispatch order changes no
+  // result: every tile sums its K products in the same order.
+  const int first_small =
+      (EPI == XEMA_EPI_GATED_RESIDUAL && p.K <= 4096) ? (int)(std::min<int64_t>(small, 192) & ~7) : 0;
   hipLaunchKernelGGL((k_gemm<T, EPI, CT, RT>), dim3((unsigned)(big + small)), dim3(NWAVES * 64), 0, s, p,
-                     split, (int)big, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
+                     split, (int)big, first_small, p.bias, (CT*)p.c, (const RT*)p.resid, p.gate);
   return hipGetLastError();
 }
 
