@@ -158,7 +158,12 @@ struct WaveState {
 // S^T - mrow for two 32-key blocks of one query column: -mrow is the
 // accumulator input of the first k-step, so the scores arrive shifted.
 // (The key fragments are the same for every column; the compiler reads them
-// from LDS once per tile.)
+// from LDS once per tile.)  The first k-step of each block is written out
+// with an early-clobber output, so that it reads minit where it lies: the
+// builtin form made the compiler copy minit into the second block's
+// accumulator on every tile (16 64-bit moves per tile and column pair, 1%
+// of the kernel).  Its result feeds the next MFMA of the same opcode as
+// that MFMA's accumulator, a dependency the compiler pads with wait states.
 template <int HD>
 __device__ __forceinline__ void scores_col(const uint8_t* Ks, const f16x8 (&qc)[HD / 16], const f32x16& minit,
                                            int krow, int kswz, int hi, f32x16 (&s)[2]) {
@@ -169,7 +174,10 @@ __device__ __forceinline__ void scores_col(const uint8_t* Ks, const f16x8 (&qc)[
     for (int kk = 0; kk < HD / 16; ++kk) {
       const int slot16 = (kk * 2 + hi) ^ kswz;
       const f16x8 kf = *reinterpret_cast<const f16x8*>(Ks + row * (HD * 2) + slot16 * 16);
-      s[kb] = mma(kf, qc[kk], kk == 0 ? minit : s[kb]);
+      if (kk == 0)
+        asm("v_mfma_f32_32x32x16_f16 %0, %1, %2, %3" : "=&v"(s[kb]) : "v"(kf), "v"(qc[kk]), "v"(minit));
+      else
+        s[kb] = mma(kf, qc[kk], s[kb]);
     }
   }
 }
