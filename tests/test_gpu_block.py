@@ -129,6 +129,24 @@ def test_batch_rows_are_independent_runs():
         assert torch.equal(o1[0], full[b]), b
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_permuting_tokens_without_rope_permutes_outputs(head_dim):
+    """P3 on the GPU: with RoPE off (rope_dims 0, 0, 0) the block is
+    equivariant under a permutation of a sequence's tokens, so the GPU's
+    output on the permuted tokens matches the permuted oracle output (within
+    the parity bar: the order of the keys in attention's sums changes)."""
+    s = W.tiny_shape(name=f"norope{head_dim}", cfg_id=64, batch=2, text_len=11, grid=(2, 6, 9), hidden=512,
+                     heads=512 // head_dim, head_dim=head_dim, mlp_hidden=1024, cond_dim=512, rope_dims=(0, 0, 0))
+    inp = W.make_inputs(s)
+    perm = np.random.default_rng(9).permutation(s.seq_len)
+    pinp = W.Inputs(s, np.ascontiguousarray(inp.x[:, perm]), inp.cond, inp.weights)
+    ref = O.block_forward_shape(inp)
+    out, _, _ = Device(inp).run(0)
+    pout, _, _ = Device(pinp).run(0)
+    assert_parity(out.cpu().numpy(), ref, f"no rope d={head_dim}")
+    assert_parity(pout.cpu().numpy(), ref[:, perm], f"permuted tokens, no rope d={head_dim}")
+
+
 # Degenerate request shapes: text only (empty grid), visual only (no text),
 # a sequence shorter than one 64-key tile, with extreme chunkings.
 EDGE = {
