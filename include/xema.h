@@ -255,11 +255,13 @@ XEMA_API int xema_dit_block_fwd(const xema_block_cfg* cfg, const xema_request* r
  * with chunking: a batch whose arena exceeds the budget can run its
  * sequences through the block in equal groups of g < batch (g divides the
  * batch), one group after another, each group seeing the arena of a
- * g-sequence request; elsewhere the batch keeps its size.  Among the
- * (g, chunk) pairs whose arena fits budget_bytes the plan takes the most
- * tokens per launch (g * chunk), then the larger g: a proxy for the least
- * latency overhead of pi* (Sec. 5.1), since launches over more tokens fill
- * the GPU better.  With an ample budget it is (batch, L): no mitigation.
+ * g-sequence request; elsewhere the batch keeps its size.  For each g the
+ * plan takes the largest chunk whose arena fits budget_bytes, and among
+ * those (g, chunk) pairs the least modelled block time, then the larger g:
+ * the least latency overhead of pi* (Sec. 5.1) under the latency model of
+ * xema_step_plan_budget (xema_step.h), the rounds of workgroups of every
+ * launch over the 256 CUs.  Groups and chunks never remove a round, so with
+ * an ample budget it is (batch, L): no mitigation.
  * *batch_group receives g and `out` the layout for a g-sequence request.
  * Host only.
  * Errors: as xema_workspace_plan; BUDGET_TOO_SMALL when even one sequence at

@@ -26,6 +26,7 @@ candidate chunk whose arena fits the budget.
 from __future__ import annotations
 
 import dataclasses
+import math
 from typing import List, Optional, Sequence, Tuple
 
 ALIGN = 256
@@ -173,13 +174,47 @@ def plan(shape, budget_bytes: int):
     return None, None, smallest
 
 
+CUS = 256  # compute units of the modelled GPU
+
+
+def block_ms(shape, group: int, chunk: int, tflops: float) -> float:
+    """Modelled time of one block in ms (the latency model, reading R30):
+    with the batch in groups of `group` sequences and chunks of `chunk`
+    tokens, the sum over its launches of the rounds of workgroups over the
+    256 CUs, a round costing one workgroup's FLOPs at tflops / 256 per CU
+    (GEMM tiles of 256 x 256; attention query blocks of 512 queries at
+    head_dim 64 and 256 at 128, each over all L keys)."""
+    s = shape
+    B, L, D, F, H, d = s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.heads, s.head_dim
+    c = L if chunk <= 0 or chunk >= L else chunk
+    qwg = 512 if d == 64 else 256
+
+    def rounds(n):
+        return math.ceil(n / CUS)
+
+    def gemm(m, n, k):
+        return rounds(math.ceil(m / 256) * (n // 256)) * 2.0 * 256 * 256 * k
+
+    flops = 0.0
+    for t0 in range(0, L, c):
+        ck = min(c, L - t0)
+        m = group * ck
+        flops += gemm(m, 3 * D, D) + gemm(m, D, D) + gemm(m, F, D) + gemm(m, D, F)
+        flops += rounds(math.ceil(ck / qwg) * H * group) * 4.0 * qwg * L * d
+    return flops * (B // group) / (tflops * 1e12 / CUS) * 1e3
+
+
+
+PLAN_TFLOPS = 1000.0  # any positive rate ranks the same
+
+
 def plan_serial(shape, budget_bytes: int):
     """Temporary serialization (Sec. 5.2) together with chunking, choosing
-    the mitigation with the least latency overhead (Sec. 5.1, pi*) by a
-    proxy: among the (g, c) whose arena fits `budget_bytes` (the batch split
-    into equal groups of g sequences run through the block one after
-    another, each in chunks of c tokens), the most tokens per launch g * c,
-    then the larger g.  Returns (g, chunk, arena bytes) or None."""
+    the mitigation with the least latency overhead (Sec. 5.1, pi*) by the
+    latency model: for each equal group size g (the batch split into groups
+    of g sequences run through the block one after another), the largest
+    chunk c whose arena fits `budget_bytes`; among those (g, c) the least
+    block_ms, then the larger g.  Returns (g, chunk, arena bytes) or None."""
     B = shape.batch
     best = None
     for g in range(B, 0, -1):
@@ -188,7 +223,8 @@ def plan_serial(shape, budget_bytes: int):
         for c in chunk_candidates(shape.seq_len):
             need = workspace_bytes(shape.with_(batch=g), c)
             if need <= budget_bytes:
-                if best is None or g * c > best[0] * best[1]:
-                    best = (g, c, need)
+                ms = block_ms(shape, g, c, PLAN_TFLOPS)
+                if best is None or ms < best[3] * (1.0 - 1e-12):
+                    best = (g, c, need, ms)
                 break
-    return best
+    return None if best is None else best[:3]

@@ -40,9 +40,9 @@ from typing import Dict, List, Optional, Tuple
 
 from . import layout as LY
 from . import offload as OF
+from .layout import block_ms  # the latency model (reading R30), shared with the block plan
 
 STEPS_PER_BLOCK = 10
-CUS = 256
 
 
 def step_tensors(shape, n_blocks: int, group: int, chunk: int, n_staging: int, slot_bytes: int,
@@ -79,27 +79,6 @@ def step_workspace(shape, n_blocks: int, group: int, chunk: int, n_staging: int,
                    weights_f16: int = 0) -> int:
     ts, _ = step_tensors(shape, n_blocks, group, chunk, n_staging, slot_bytes, weights_f16)
     return LY.static_layout(ts)[1]
-
-
-def block_ms(shape, group: int, chunk: int, tflops: float) -> float:
-    s = shape
-    B, L, D, F, H, d = s.batch, s.seq_len, s.hidden, s.mlp_hidden, s.heads, s.head_dim
-    c = L if chunk <= 0 or chunk >= L else chunk
-    qwg = 512 if d == 64 else 256
-
-    def rounds(n):
-        return math.ceil(n / CUS)
-
-    def gemm(m, n, k):
-        return rounds(math.ceil(m / 256) * (n // 256)) * 2.0 * 256 * 256 * k
-
-    flops = 0.0
-    for t0 in range(0, L, c):
-        ck = min(c, L - t0)
-        m = group * ck
-        flops += gemm(m, 3 * D, D) + gemm(m, D, D) + gemm(m, F, D) + gemm(m, D, F)
-        flops += rounds(math.ceil(ck / qwg) * H * group) * 4.0 * qwg * L * d
-    return flops * (B // group) / (tflops * 1e12 / CUS) * 1e3
 
 
 def step_ms(n_blocks: int, offloaded: List[int], n_staging: int, t_blk: float, t_x: float) -> float:

@@ -238,6 +238,10 @@ extern "C" int xema_workspace_plan(const xema_block_cfg* cfg, const xema_request
   return XEMA_ERR_BUDGET_TOO_SMALL;
 }
 
+// The rate the ranking of xema_workspace_plan_serial assumes; any positive
+// value gives the same ranking, since the model's time is proportional to it.
+constexpr double kPlanTflops = 1000.0;
+
 extern "C" int xema_workspace_plan_serial(const xema_block_cfg* cfg, const xema_request* req,
                                           int64_t budget_bytes, int32_t* batch_group,
                                           xema_plan* out) {
@@ -249,22 +253,26 @@ extern "C" int xema_workspace_plan_serial(const xema_block_cfg* cfg, const xema_
   std::vector<int64_t> cands{L};
   for (int64_t c = (L - 1) / XEMA_CHUNK_GRANULE * XEMA_CHUNK_GRANULE; c > 0; c -= XEMA_CHUNK_GRANULE)
     cands.push_back(c);
-  // Among the (g, c) whose arena fits, the most tokens per launch (g * c),
-  // then the larger group: the launches that fill the GPU best.  With the
-  // budget ample this is (batch, L), no mitigation at all.
-  int64_t best_tokens = 0;
+  // For each group size g the largest chunk whose arena fits (a smaller
+  // chunk never shortens the modelled time); among those the least modelled
+  // time of the block (block_ms), then the larger g.  Neither groups nor
+  // chunks ever remove a round of the model, so with an ample budget this
+  // is (batch, L): no mitigation at all.
+  double best_ms = 0.0;
   for (int32_t g = req->batch; g >= 1; --g) {
     if (req->batch % g) continue;  // equal groups only
     xema_request rg = *req;
     rg.batch = g;
     for (int64_t c : cands) {
-      if ((int64_t)g * c <= best_tokens) break;  // candidates shrink: nothing better below
       xema_plan pg;
       layout_for_chunk(*cfg, rg, c, &pg);
       if (pg.workspace_bytes <= budget_bytes) {
-        *out = pg;
-        *batch_group = g;
-        best_tokens = (int64_t)g * c;
+        const double ms = block_ms(*cfg, *req, g, c, kPlanTflops);
+        if (*batch_group == 0 || ms < best_ms * (1.0 - 1e-12)) {
+          *out = pg;
+          *batch_group = g;
+          best_ms = ms;
+        }
         break;  // the largest fitting chunk for this g
       }
     }

@@ -113,12 +113,6 @@ int step_layout(const xema_block_cfg& c, const xema_request& r, int n_blocks, in
   return XEMA_OK;
 }
 
-namespace {
-
-bool costs_ok(const xema_step_costs* k) {
-  return k && k->h2d_gbytes_per_s > 0.0 && k->block_tflops > 0.0;
-}
-
 // Modelled time of one block (all its groups and chunks), milliseconds: the
 // rounds of workgroups of each launch over the 256 CUs, a round costing one
 // workgroup's FLOPs at block_tflops / 256 per CU.
@@ -136,6 +130,12 @@ double block_ms(const xema_block_cfg& c, const xema_request& r, int64_t g, int64
     flops += rounds((ck + qwg - 1) / qwg * H * g) * 4.0 * (double)qwg * (double)L * (double)d;
   }
   return flops * (double)(B / g) / (tflops * 1e12 / 256.0) * 1e3;
+}
+
+namespace {
+
+bool costs_ok(const xema_step_costs* k) {
+  return k && k->h2d_gbytes_per_s > 0.0 && k->block_tflops > 0.0;
 }
 
 // End of the last block: the copy stream runs the copies of the offloaded

@@ -80,6 +80,13 @@ struct StepLayout {
 };
 int step_layout(const xema_block_cfg& c, const xema_request& r, int n_blocks, int group, int64_t chunk,
                 int n_staging, int64_t slot_bytes, StepLayout* out);
+// Modelled time of one block, milliseconds, with the batch in groups of g
+// sequences and chunks of ch tokens: the rounds of workgroups of each launch
+// over the 256 CUs, a round costing one workgroup's FLOPs at tflops / 256 per
+// CU (the latency model of the step plan; xema_workspace_plan_serial ranks
+// by it too).
+double block_ms(const xema_block_cfg& c, const xema_request& r, int64_t g, int64_t ch, double tflops);
+
 // xema_step_plan_fixed without the argument checks.
 int make_step_plan(const xema_block_cfg& c, const xema_request& r, int n_blocks, int n_offloaded, int n_staging,
                    int group, int64_t chunk, const xema_step_costs& costs, xema_step_plan* out);

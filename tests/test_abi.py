@@ -103,8 +103,9 @@ def test_highres_32gb_budget_runs_unchunked():
 
 @pytest.mark.parametrize("name", ["image_b4", "long", "tiny"])
 def test_serial_plan_matches_oracle(name):
-    """Temporary serialization: the largest group size, then the largest
-    chunk, that fits; only when chunking alone cannot fit the whole batch."""
+    """Temporary serialization: per group size the largest chunk that fits,
+    then the least modelled block time (oracle.layout.block_ms); the batch
+    stays whole when chunking alone fits it at no modelled cost."""
     s = W.CONFIGS[name]
     cfg, req = _cfg(s), _req(s)
     cands = OL.chunk_candidates(s.seq_len)
