@@ -280,6 +280,10 @@ def test_workload_parity_full_output(name):
 
 
 def test_video_chunks_are_bit_identical_at_full_size():
+    """At the full video size: chunked runs give the unchunked bytes, and so
+    does the configuration bench.py times (W_o, W_up, W_down handed over in
+    fp16, the pipelined entry point with a second stream), which ties the
+    bench's launches to the full-output parity test above."""
     s = W.VIDEO
     dev = Device(W.make_inputs(s))
     base, _, _ = dev.run(0)
@@ -289,6 +293,19 @@ def test_video_chunks_are_bit_identical_at_full_size():
         assert plan.chunk_tokens == chunk
         assert torch.equal(out, base), chunk
     del dev
+    torch.cuda.empty_cache()
+    print("video, fp16 phase-B weights, pipelined entry point, against unchunked", flush=True)
+    dev16 = Device(W.make_inputs(s.with_(weights_f16=1)))
+    group, plan = X.xema_workspace_plan_serial(dev16.cfg, dev16.req, 2 << 30)
+    assert (group, plan.chunk_tokens) == (1, s.seq_len)
+    ws = poison(torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV))
+    out = poison(torch.empty_like(base))
+    X.xema_dit_block_fwd_pipelined(dev16.cfg, dev16.req, dev16.x, dev16.weights, dev16.cond, group,
+                                   plan.chunk_tokens, ws, ws.numel(), out, None, torch.cuda.Stream())
+    torch.cuda.synchronize()
+    assert X.xema_block_status(plan, ws) == 0
+    assert torch.equal(out, base)
+    del dev16, ws, out
     torch.cuda.empty_cache()
 
 
