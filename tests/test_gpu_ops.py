@@ -258,9 +258,10 @@ def test_qk_norm_rope_matches_oracle(head_dim, rope_dims, grid, text_len):
     assert np.all(got[..., L:] == 0)
 
 
-def _attention_case(qs, k, v, q0, qn, what):
+def _attention_case(qs, k, v, q0, qn, what, ref=None):
     """Run the attention op on queries pre-multiplied by log2(e)/sqrt(d)
-    (weights 2^(qs . k)) and compare with the oracle."""
+    (weights 2^(qs . k)) and compare with `ref` ([B, qn, H, d]), by default
+    the oracle's."""
     B, H, L, head_dim = qs.shape
     Lp = X.padded_len(L)
     q = qs.astype(np.float64) * (np.sqrt(head_dim) / LOG2E)
@@ -274,11 +275,12 @@ def _attention_case(qs, k, v, q0, qn, what):
     X.xema_op_attention(qd, kd, vtd, B, H, head_dim, L, Lp, q0, qn, o)
     torch.cuda.synchronize()
     got = o.float().cpu().numpy().reshape(B, qn, H, head_dim)
-    ref = np.empty((B, qn, H, head_dim))
-    for b in range(B):
-        for h in range(H):
-            ref[b, :, h] = O.attention(q[b, h, q0:q0 + qn], k[b, h].astype(np.float64),
-                                       v[b, h].astype(np.float64))
+    if ref is None:
+        ref = np.empty((B, qn, H, head_dim))
+        for b in range(B):
+            for h in range(H):
+                ref[b, :, h] = O.attention(q[b, h, q0:q0 + qn], k[b, h].astype(np.float64),
+                                           v[b, h].astype(np.float64))
     _check_close(got, ref, 2.0 ** -9, 2e-3, what)
 
 
@@ -318,6 +320,22 @@ def test_attention_rescaling(head_dim, profile):
     qs, k = _f16(qs), _f16(k)
     v = _f16(g.standard_normal((B, H, L, head_dim)))
     _attention_case(qs, k, v, 0, L, f"attention d={head_dim} rescaling profile {profile}")
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_attention_equal_keys_average_v(head_dim):
+    """P10 on the GPU, against the closed form rather than the oracle: with
+    every key of a head equal, all scores of a query are equal and its output
+    is the mean of the head's V rows (1000 keys: fifteen full tiles and a
+    ragged tail)."""
+    B, H, L = 1, 2, 1000
+    g = _rng(400 + head_dim)
+    qs = _f16(g.standard_normal((B, H, L, head_dim)) * (LOG2E / np.sqrt(head_dim)))
+    k = np.ascontiguousarray(np.repeat(_f16(g.standard_normal((B, H, 1, head_dim))), L, axis=2))
+    v = _f16(g.standard_normal((B, H, L, head_dim)))
+    mean_v = v.astype(np.float64).mean(axis=2)                      # [B, H, d]
+    ref = np.broadcast_to(mean_v[:, None, :, :], (B, L, H, head_dim))
+    _attention_case(qs, k, v, 0, L, f"attention d={head_dim}, equal keys", ref)
 
 
 def test_attention_queries_independent_of_range():
