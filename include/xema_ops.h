@@ -7,6 +7,13 @@
  * any launch, caller-owned device buffers, no allocation, asynchronous on
  * `stream` (a hipStream_t, NULL = default stream), 16-byte aligned pointers.
  * Element types are given by xema_dtype codes.
+ *
+ * fp16 outputs (y of xema_op_ln_modulate and c of xema_op_gemm with
+ * XEMA_F16, q, k and vt of xema_op_qk_norm_rope, o of xema_op_attention,
+ * dst of xema_op_convert_f16) have the fp16 range of +-65504 that xema.h's
+ * precision contract states: larger values round to +-inf.  These
+ * single-step entry points do not check it (no range flags); the block
+ * entry points of xema.h do, through xema_block_status.
  */
 #ifndef XEMA_OPS_H_
 #define XEMA_OPS_H_
