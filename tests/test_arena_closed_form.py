@@ -29,7 +29,7 @@ Lp = L rounded up to 128, S = 2 modulation maps for a dual-stream block else 1.
 
   arena(c) = always + max(phase A, phase B)
 
-Against the survey's proposal, arena(c) = 6 B L D + B c max(8D, 6D + 2F) +
+Against the simpler estimate arena(c) = 6 B L D + B c max(8D, 6D + 2F) +
 24 B D, this adds the 128-token padding of Q/K/V, the RoPE table, the status
 words and the weight copies, drops the qkv intermediate (8D -> 2D per token
 in phase A) and keeps the attention rows live when chunked.  Algorithm 1
